@@ -1,0 +1,314 @@
+"""Pins of the encoder oracle against things other than itself.
+
+* a library encoder (``transformers.BertModel``, float64, eager attention)
+  loaded with the oracle's weights, run on a padded batch with an attention
+  mask, followed by masked mean pooling and L2 normalisation;
+* brute-force attention on a padded batch with an additive -inf mask;
+* closed forms and invariants (zero sublayers, repeated tokens, permutation
+  invariance without positions, single-token attention, textbook GELU
+  values, unit norm, invariance under SuperBatch composition).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import encoder as E
+from paper_2605_01060_amd import workload as W
+
+SMALL_DH32 = W.EncoderShape(2, 96, 3, 192, 30522, 40, "f32")  # d_head = 32
+SMALL_DH64 = W.EncoderShape(2, 128, 2, 512, 30522, 64, "f32")  # the tiny config
+
+
+def _weights(shape, seed=0, init="random"):
+    return E.as_f64(W.make_weights(shape, seed=seed, init=init))
+
+
+def _texts(lengths, seed=3):
+    rng = np.random.default_rng(seed)
+    out = []
+    for L in lengths:
+        ids = rng.integers(W.TOKEN_LO, W.TOKEN_HI, size=L, endpoint=True)
+        ids[0] = W.CLS_ID
+        ids[-1] = W.SEP_ID if L > 1 else ids[-1]
+        out.append(ids.astype(np.int64))
+    return out
+
+
+def _bert_embeddings(shape, w, texts):
+    torch = pytest.importorskip("torch")
+    transformers = pytest.importorskip("transformers")
+    cfg = transformers.BertConfig(
+        vocab_size=shape.vocab_size, hidden_size=shape.d_model,
+        num_hidden_layers=shape.n_layers, num_attention_heads=shape.n_heads,
+        intermediate_size=shape.d_ff, hidden_act="gelu",
+        max_position_embeddings=shape.max_positions, type_vocab_size=1,
+        layer_norm_eps=shape.ln_eps, hidden_dropout_prob=0.0,
+        attention_probs_dropout_prob=0.0)
+    cfg._attn_implementation = "eager"
+    model = transformers.BertModel(cfg, add_pooling_layer=False).double().eval()
+    d = shape.d_model
+    sd = {
+        "embeddings.word_embeddings.weight": w["word_emb"],
+        "embeddings.position_embeddings.weight": w["pos_emb"],
+        "embeddings.token_type_embeddings.weight": np.zeros((1, d)),
+        "embeddings.LayerNorm.weight": w["ln_e_g"],
+        "embeddings.LayerNorm.bias": w["ln_e_b"],
+    }
+    for l in range(shape.n_layers):
+        p, q = f"layer{l}.", f"encoder.layer.{l}."
+        wq = w[p + "w_qkv"]
+        bq = w[p + "b_qkv"]
+        for j, nm in enumerate(("query", "key", "value")):
+            sd[q + f"attention.self.{nm}.weight"] = wq[:, j * d:(j + 1) * d].T
+            sd[q + f"attention.self.{nm}.bias"] = bq[j * d:(j + 1) * d]
+        sd[q + "attention.output.dense.weight"] = w[p + "w_o"].T
+        sd[q + "attention.output.dense.bias"] = w[p + "b_o"]
+        sd[q + "attention.output.LayerNorm.weight"] = w[p + "ln1_g"]
+        sd[q + "attention.output.LayerNorm.bias"] = w[p + "ln1_b"]
+        sd[q + "intermediate.dense.weight"] = w[p + "w_1"].T
+        sd[q + "intermediate.dense.bias"] = w[p + "b_1"]
+        sd[q + "output.dense.weight"] = w[p + "w_2"].T
+        sd[q + "output.dense.bias"] = w[p + "b_2"]
+        sd[q + "output.LayerNorm.weight"] = w[p + "ln2_g"]
+        sd[q + "output.LayerNorm.bias"] = w[p + "ln2_b"]
+    state = {k: torch.tensor(np.ascontiguousarray(v), dtype=torch.float64) for k, v in sd.items()}
+    missing, unexpected = model.load_state_dict(state, strict=False)
+    assert not unexpected
+    assert all("position_ids" in m or "token_type_ids" in m for m in missing), missing
+    Lmax = max(len(t) for t in texts)
+    ids = np.zeros((len(texts), Lmax), dtype=np.int64)
+    mask = np.zeros((len(texts), Lmax), dtype=np.int64)
+    for i, t in enumerate(texts):
+        ids[i, :len(t)] = t
+        mask[i, :len(t)] = 1
+    with torch.no_grad():
+        hs = model(input_ids=torch.tensor(ids), attention_mask=torch.tensor(mask),
+                   token_type_ids=torch.zeros_like(torch.tensor(ids))).last_hidden_state.numpy()
+    m = mask[:, :, None].astype(np.float64)
+    mean = (hs * m).sum(axis=1) / m.sum(axis=1)
+    return mean / np.maximum(np.linalg.norm(mean, axis=1, keepdims=True), 1e-12)
+
+
+@pytest.mark.parametrize("shape", [SMALL_DH64, SMALL_DH32], ids=["dh64", "dh32"])
+def test_matches_library_bert_encoder(shape):
+    w = _weights(shape, seed=11)
+    lengths = [1, 2, 3, 7, 16, 17, shape.max_positions]
+    texts = _texts(lengths)
+    ref = _bert_embeddings(shape, w, texts)
+    got = np.stack([E.encode_text(w, shape.n_layers, shape.n_heads, t, shape.ln_eps)
+                    for t in texts])
+    assert np.max(np.abs(got - ref)) < 1e-10
+
+
+def test_matches_library_bert_encoder_bert_init():
+    shape = SMALL_DH64
+    w = _weights(shape, seed=5, init="bert")
+    texts = _texts([4, 9, 33])
+    ref = _bert_embeddings(shape, w, texts)
+    got = np.stack([E.encode_text(w, shape.n_layers, shape.n_heads, t) for t in texts])
+    assert np.max(np.abs(got - ref)) < 1e-10
+
+
+def _padded_bruteforce_attention(qkv_list, n_heads):
+    """Dense attention on a padded batch [n, Lmax, 3d] with an additive -inf mask."""
+    n = len(qkv_list)
+    Lmax = max(a.shape[0] for a in qkv_list)
+    three_d = qkv_list[0].shape[1]
+    d = three_d // 3
+    dh = d // n_heads
+    X = np.zeros((n, Lmax, three_d))
+    valid = np.zeros((n, Lmax), dtype=bool)
+    for i, a in enumerate(qkv_list):
+        X[i, :a.shape[0]] = a
+        valid[i, :a.shape[0]] = True
+    q = X[..., :d].reshape(n, Lmax, n_heads, dh).transpose(0, 2, 1, 3)
+    k = X[..., d:2 * d].reshape(n, Lmax, n_heads, dh).transpose(0, 2, 1, 3)
+    v = X[..., 2 * d:].reshape(n, Lmax, n_heads, dh).transpose(0, 2, 1, 3)
+    s = np.einsum("nhqe,nhke->nhqk", q, k) * (dh ** -0.5)
+    s = s + np.where(valid[:, None, None, :], 0.0, -np.inf)
+    s = s - s.max(axis=-1, keepdims=True)
+    p = np.exp(s)
+    p = p / p.sum(axis=-1, keepdims=True)
+    o = np.einsum("nhqk,nhke->nhqe", p, v).transpose(0, 2, 1, 3).reshape(n, Lmax, d)
+    return [o[i, :a.shape[0]] for i, a in enumerate(qkv_list)]
+
+
+@pytest.mark.parametrize("n_heads,d", [(2, 128), (3, 96), (4, 64)])
+def test_attention_matches_padded_bruteforce(n_heads, d):
+    rng = np.random.default_rng(7)
+    lengths = [1, 2, 5, 8, 13, 16, 3, 11]
+    qkv = [rng.standard_normal((L, 3 * d)) for L in lengths]
+    ref = _padded_bruteforce_attention(qkv, n_heads)
+    for a, r in zip(qkv, ref):
+        got = E.self_attention(a, n_heads)
+        assert np.max(np.abs(got - r)) < 1e-12
+
+
+def test_attention_single_key_returns_value_row():
+    rng = np.random.default_rng(1)
+    qkv = rng.standard_normal((1, 3 * 64))
+    out = E.self_attention(qkv, 2)
+    assert np.array_equal(out[0], qkv[0, 128:])
+
+
+def test_attention_with_zero_queries_is_mean_of_values():
+    # W_Q = W_K = 0, b_Q = b_K = 0: every score is 0, so every row attends
+    # uniformly and returns the mean of the text's V rows.
+    rng = np.random.default_rng(2)
+    L, d = 9, 64
+    qkv = rng.standard_normal((L, 3 * d))
+    qkv[:, :2 * d] = 0.0
+    out = E.self_attention(qkv, 4)
+    expect = np.broadcast_to(qkv[:, 2 * d:].mean(axis=0), (L, d))
+    assert np.max(np.abs(out - expect)) < 1e-14
+
+
+def test_attention_is_softmax_weighted_and_scaled():
+    # Two keys, one query, d_head = 4: weights are the 2-way softmax of
+    # (q.k_j)/2, a logistic function of the score difference.
+    q = np.array([1.0, 0.0, 0.0, 0.0])
+    k0 = np.array([2.0, 0.0, 0.0, 0.0])
+    k1 = np.array([0.0, 0.0, 0.0, 0.0])
+    v0 = np.array([1.0, 0.0, 0.0, 0.0])
+    v1 = np.array([0.0, 1.0, 0.0, 0.0])
+    qkv = np.stack([np.concatenate([q, k0, v0]), np.concatenate([q, k1, v1])])
+    out = E.self_attention(qkv, 1)
+    w0 = 1.0 / (1.0 + np.exp(-1.0))  # score difference (2 - 0) / sqrt(4) = 1
+    assert np.allclose(out[0], [w0, 1 - w0, 0, 0], atol=1e-15)
+
+
+def test_gelu_textbook_values(golden_dir):
+    pts = json.load(open(os.path.join(golden_dir, "normal_cdf.json")))["points"]
+    for x, phi in pts:
+        assert abs(E.gelu(np.array(x)) - x * phi) < 1e-15
+
+
+def test_layer_norm_closed_forms():
+    x = np.array([[1.0, 2.0, 3.0, 4.0]])
+    out = E.layer_norm(x, np.ones(4), np.zeros(4), 0.0)
+    s = np.sqrt(1.25)
+    assert np.allclose(out, [[-1.5 / s, -0.5 / s, 0.5 / s, 1.5 / s]], atol=1e-15)
+    g = np.array([2.0, 1.0, 1.0, 0.5])
+    b = np.array([0.0, 1.0, -1.0, 3.0])
+    out2 = E.layer_norm(x + 10.0, g, b, 0.0)
+    assert np.allclose(out2, g * out + b, atol=1e-14)
+    # eps enters as var + eps: a constant row maps to beta.
+    assert np.allclose(E.layer_norm(np.full((1, 4), 3.0), g, b, 1e-12), b)
+
+
+def test_zero_sublayers_reduce_to_standardized_embeddings():
+    # All layer matrices and biases zero, gamma = 1, beta = 0: each sublayer
+    # output is zero, so every post-LN step only re-standardises its input.
+    shape = SMALL_DH64
+    w = _weights(shape, seed=4)
+    for l in range(shape.n_layers):
+        for t in W.LAYER_TENSORS:
+            k = f"layer{l}.{t}"
+            w[k] = np.ones_like(w[k]) if t.endswith("_g") else np.zeros_like(w[k])
+    ids = _texts([12])[0]
+    z = w["word_emb"][ids] + w["pos_emb"][:12]
+    z = (z - z.mean(1, keepdims=True)) / np.sqrt(z.var(1, keepdims=True) + 1e-12)
+    z = w["ln_e_g"] * z + w["ln_e_b"]
+    z = (z - z.mean(1, keepdims=True)) / np.sqrt(z.var(1, keepdims=True) + 1e-12)
+    e = z.mean(0)
+    e = e / np.linalg.norm(e)
+    got = E.encode_text(w, shape.n_layers, shape.n_heads, ids)
+    assert np.max(np.abs(got - e)) < 1e-9
+
+
+def test_repeated_token_without_positions_is_length_invariant():
+    # W_pos = 0: a text made of one repeated token has identical rows at every
+    # layer (attention over identical V rows returns that row), so its
+    # embedding does not depend on its length.
+    shape = SMALL_DH64
+    w = _weights(shape, seed=8)
+    w["pos_emb"] = np.zeros_like(w["pos_emb"])
+    ref = E.encode_text(w, shape.n_layers, shape.n_heads, np.array([4242]))
+    for L in (2, 5, 31, 64):
+        got = E.encode_text(w, shape.n_layers, shape.n_heads, np.full(L, 4242))
+        assert np.max(np.abs(got - ref)) < 1e-12
+
+
+def test_permutation_invariance_without_positions():
+    # Without position embeddings the encoder is permutation-equivariant and
+    # mean pooling is symmetric, so shuffling a text's tokens keeps its
+    # embedding; any position-dependent masking would break this.
+    shape = SMALL_DH32
+    w = _weights(shape, seed=9)
+    w["pos_emb"] = np.zeros_like(w["pos_emb"])
+    ids = _texts([23])[0]
+    perm = np.random.default_rng(0).permutation(23)
+    a = E.encode_text(w, shape.n_layers, shape.n_heads, ids)
+    b = E.encode_text(w, shape.n_layers, shape.n_heads, ids[perm])
+    assert np.max(np.abs(a - b)) < 1e-12
+
+
+def test_positions_matter():
+    shape = SMALL_DH32
+    w = _weights(shape, seed=9)
+    ids = _texts([23])[0]
+    perm = np.random.default_rng(0).permutation(23)
+    a = E.encode_text(w, shape.n_layers, shape.n_heads, ids)
+    b = E.encode_text(w, shape.n_layers, shape.n_heads, ids[perm])
+    assert np.max(np.abs(a - b)) > 1e-3
+
+
+def test_unit_norm_and_placement_on_tiny_workload():
+    spec = W.WORKLOADS["tiny"]
+    wl = W.make_workload(spec)
+    shape = spec.encoder
+    w = _weights(shape)
+    n = 120
+    sub_sizes = []
+    offs = wl.part_offsets
+    for p in range(len(offs) - 1):
+        lo, hi = min(offs[p], n), min(offs[p + 1], n)
+        sub_sizes.append(hi - lo)
+    sub_offsets = np.concatenate([[0], np.cumsum(sub_sizes)])
+    parts = E.encode_workload(w, shape.n_layers, shape.n_heads, wl.tokens,
+                              wl.cu_seqlens[:n + 1], sub_offsets)
+    assert [p.shape[0] for p in parts] == sub_sizes
+    flat = np.concatenate(parts)
+    assert np.max(np.abs(np.linalg.norm(flat, axis=1) - 1.0)) < 1e-12
+    alone = E.encode_texts(w, shape.n_layers, shape.n_heads, wl.tokens,
+                           wl.cu_seqlens, [0, 57, 119])
+    assert np.array_equal(flat[[0, 57, 119]], alone)
+
+
+def test_placement_closed_form():
+    offs = np.array([0, 3, 3, 7, 8, 8, 10])
+    expect = []
+    for p in range(len(offs) - 1):
+        for r in range(offs[p + 1] - offs[p]):
+            expect.append((p, r))
+    assert [E.placement(offs, i) for i in range(10)] == expect
+
+
+def test_invariance_under_composition():
+    # The embedding of a text is a function of its own tokens only: encoding
+    # it alone, inside a different selection, or in reversed order gives the
+    # same bits.
+    spec = W.WORKLOADS["tiny"]
+    wl = W.make_workload(spec)
+    shape = spec.encoder
+    w = _weights(shape)
+    idx = [5, 6, 7, 300, 999]
+    a = E.encode_texts(w, shape.n_layers, shape.n_heads, wl.tokens, wl.cu_seqlens, idx)
+    b = E.encode_texts(w, shape.n_layers, shape.n_heads, wl.tokens, wl.cu_seqlens, idx[::-1])
+    assert np.array_equal(a, b[::-1])
+
+
+def test_discrimination_record():
+    # Test validity: random-init embeddings of different texts must not all
+    # coincide, or parity tests would have no teeth.
+    spec = W.WORKLOADS["tiny"]
+    wl = W.make_workload(spec)
+    shape = spec.encoder
+    w = _weights(shape)
+    e = E.encode_texts(w, shape.n_layers, shape.n_heads, wl.tokens, wl.cu_seqlens, range(40))
+    c = e @ e.T
+    off = c[~np.eye(40, dtype=bool)]
+    assert np.median(off) < 0.8
+    assert off.max() < 0.99
