@@ -1,0 +1,208 @@
+"""Benchmark: SuperBatch encoding throughput on one MI355X.
+
+A step is one pass of the whole encode path (SuperBatch formation, packing
+metadata, embedding, every encoder layer, pooling, L2 and partition scatter)
+over the whole synthetic workload, via surge_encode_all with inputs already
+resident in HBM.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload bge] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2605_01060_amd import surge as S  # noqa: E402
+from paper_2605_01060_amd import workload as W  # noqa: E402
+
+METRIC = "texts/sec + MFMA util % on 1 MI355X, bge-base-shaped encoder, σ=1.72 parts"
+PEAK_BF16_TFLOPS = 2516.6  # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+MFMA_KERNELS = ("qkv", "oproj", "ffn1", "ffn2")
+
+DESCRIPTIONS = {
+    "tiny": "tiny encoder (2 L, d 128), 1,000 texts / 20 partitions, sigma 1.72, B_min 1,000",
+    "minilm": "MiniLM-L6-shaped encoder (6 L, d 384), 100k texts / 400 partitions, sigma 1.72, "
+              "B_min 4,096, n_max 20,000",
+    "bge": "bge-base-shaped encoder (12 L, d 768, 12 H, FFN 3072), 200k texts / 800 partitions, "
+           "partition sizes log-normal sigma 1.72, lengths log-normal median 48 in [4, 256], "
+           "B_min 4,096, n_max 20,000",
+    "bge_s1": "bge-base-shaped encoder, 200k texts / 800 partitions, sigma 1.0, B_min 4,096, "
+              "n_max 20,000",
+    "minilm_heavy": "MiniLM-L6-shaped encoder, 1M texts / 4,000 partitions, sigma 2.5, "
+                    "B_min 8,192, n_max 50,000",
+    "large": "~335M encoder (24 L, d 1024), 100k texts / 400 partitions, sigma 1.72, "
+             "B_min 2,048, n_max 10,000",
+}
+
+
+def encoder_flops(shape: W.EncoderShape, lengths: np.ndarray) -> float:
+    """Algorithmic matmul FLOPs: per text n_layers [2 L (4 d^2 + 2 d d_ff) + 4 d L^2]
+    (QKV, O, FFN1, FFN2, Q K^T, P V over the text's own tokens and pairs)."""
+    L = lengths.astype(np.float64)
+    d, f = shape.d_model, shape.d_ff
+    return float(shape.n_layers * (2.0 * L * (4 * d * d + 2 * d * f) + 4.0 * d * L * L).sum())
+
+
+def cpu_baseline(spec, wl, weights, budget_s: float):
+    """The oracle, as it stands, on the first texts of SuperBatch 0."""
+    from oracle import encoder as E
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    sh = spec.encoder
+    w64 = E.as_f64(weights)
+    n = 0
+    toks = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s and n < wl.n_texts:
+        ids = wl.tokens[wl.cu_seqlens[n]:wl.cu_seqlens[n + 1]]
+        E.encode_text(w64, sh.n_layers, sh.n_heads, ids, sh.ln_eps)
+        toks += len(ids)
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "texts/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} texts ({toks} tokens) of SuperBatch 0 of the same workload, "
+                      f"fp64 NumPy oracle, one text at a time, {dt:.1f} s",
+            "tokens_per_s": toks / dt}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="bge", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--chunk-tokens", type=int, default=1 << 18)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-events", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this path runs on one GPU; --gpus must be 1 "
+                                   "(SuperBatches shard across GPUs with no exchange step, "
+                                   "but multi-GPU runs are not part of this build)"}))
+        return 2
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    spec = W.WORKLOADS[args.workload]
+    sh = spec.encoder
+    wl = W.make_workload(spec)
+    weights = W.make_weights(sh, seed=spec.seed)
+    desc = S.make_desc(sh.n_layers, sh.d_model, sh.n_heads, sh.d_ff, sh.vocab_size,
+                       sh.max_positions, sh.ln_eps)
+    enc = S.Encoder(desc, [weights[n] for n in W.weight_names(sh.n_layers)], args.chunk_tokens)
+    tok = torch.from_numpy(wl.tokens).cuda()
+    out = torch.empty((wl.n_texts, sh.d_model), dtype=torch.float32, device="cuda")
+    ptrs = np.array([out.data_ptr() + int(o) * sh.d_model * 4 for o in wl.part_offsets[:-1]],
+                    dtype=np.uint64)
+    stream = torch.cuda.current_stream()
+    flops = encoder_flops(sh, wl.lengths)
+
+    def step():
+        return enc.encode_all(wl.n_texts, tok, wl.cu_seqlens, wl.part_offsets, spec.b_min,
+                              spec.n_max, ptrs, stream=stream)
+
+    for _ in range(args.warmup):
+        n_sb = step()
+    enc.check(stream)
+    torch.cuda.synchronize()
+    print(f"[bench] workload={args.workload} texts={wl.n_texts} tokens={wl.n_tokens} "
+          f"warmup done", file=sys.stderr, flush=True)
+
+    enc.profile(not args.no_kernel_events)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        n_sb = step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    enc.check(stream)
+    kstats = enc.profile_read() if not args.no_kernel_events else {}
+    enc.profile(False)
+
+    ms_step = ms / args.steps
+    texts_s = wl.n_texts / (ms_step / 1e3)
+    tflops = flops / (ms_step / 1e3) / 1e12
+    kernels = {}
+    for name, s in kstats.items():
+        if s["launches"] == 0:
+            continue
+        avg = s["total_ms"] / s["launches"]
+        ent = {"launches": s["launches"], "total_ms_per_step": s["total_ms"] / args.steps,
+               "avg_ms": avg}
+        if s["flops"] > 0:
+            ent["tflops"] = s["flops"] / (s["total_ms"] / 1e3) / 1e12
+        if s["bytes"] > 0:
+            ent["gbs"] = s["bytes"] / (s["total_ms"] / 1e3) / 1e9
+        kernels[name] = ent
+    roofline = None
+    if kernels:
+        dom = max(kernels, key=lambda k: kernels[k]["total_ms_per_step"])
+        s = kstats[dom]
+        if dom in MFMA_KERNELS:
+            achieved = s["flops"] / (s["total_ms"] / 1e3) / 1e12
+            roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
+                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                        "per_launch_flops": s["flops"] / s["launches"],
+                        "avg_launch_ms": s["total_ms"] / s["launches"]}
+        else:
+            achieved = s["bytes"] / (s["total_ms"] / 1e3) / 1e9
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved,
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                        "traffic": None, "per_launch_bytes": s["bytes"] / s["launches"],
+                        "avg_launch_ms": s["total_ms"] / s["launches"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(spec, wl, weights, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC,
+        "value": texts_s,
+        "unit": "texts/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded workload and random-init weights of the named shape)",
+        "config": {"workload": DESCRIPTIONS[args.workload], "name": args.workload,
+                   "n_texts": wl.n_texts, "n_tokens": wl.n_tokens, "n_superbatches": n_sb,
+                   "chunk_tokens": args.chunk_tokens},
+        "tokens_per_s": wl.n_tokens / (ms_step / 1e3),
+        "encoder_tflops": tflops,
+        "mfma_util_pct": 100.0 * tflops / PEAK_BF16_TFLOPS,
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    enc.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

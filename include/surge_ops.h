@@ -1,0 +1,73 @@
+/*
+ * surge_ops.h - stage-level entry points of the SuperBatch encoder.
+ *
+ * Each call runs one stage of the encode path on caller-provided device
+ * buffers, with the same kernels surge_encode_superbatch launches, so every
+ * stage can be checked on its own.  The call is synchronous: it enqueues on
+ * `hip_stream` (NULL = null stream) and waits for it before returning.
+ * bf16 tensors are passed as uint16_t bit patterns.  Text boundaries are
+ * given as host int64 cu_seqlens [n_texts+1] (cu[0] = 0, increasing), checked
+ * on the host and copied to the device by the call.  Returns the status
+ * codes of surge.h.
+ */
+#ifndef SURGE_OPS_H_
+#define SURGE_OPS_H_
+
+#include <stdint.h>
+
+#include "surge.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * Embedding gather + LayerNorm (encoder input; positions restart at 0 for
+ * every text): out[t] = LN(word[id_t] + pos[t - cu_i]).
+ * d_tokens int32 [cu[n]]; d_word bf16 [vocab, d]; d_pos bf16 [max_pos, d];
+ * gamma/beta fp32 [d]; d_out bf16 [cu[n], d].  d % 128 == 0, d <= 1024,
+ * every text length <= max_pos.  Out-of-vocabulary IDs are read as ID 0 and
+ * reported with SURGE_ERR_INVALID_ARGUMENT after the stage ran.
+ */
+surge_status surge_op_embed_ln(int64_t n_texts, const int64_t* h_cu_seqlens, const int32_t* d_tokens,
+                               const uint16_t* d_word, int32_t vocab, const uint16_t* d_pos,
+                               int32_t max_pos, const float* d_gamma, const float* d_beta,
+                               float eps, int32_t d, uint16_t* d_out, void* hip_stream);
+
+/*
+ * Linear layer over packed tokens: Y = epi(X W^T + b).
+ * d_x bf16 [M, K]; d_w bf16 [N, K] (out, in); d_bias fp32 [N];
+ * epilogue 0 = bias, 1 = bias then exact GELU, 2 = bias then + d_res
+ * (bf16 [M, N]); d_y bf16 [M, N].  M >= 1, N % 128 == 0, K % 64 == 0.
+ */
+surge_status surge_op_linear(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                             const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
+                             int32_t epilogue, uint16_t* d_y, void* hip_stream);
+
+/*
+ * Packed varlen multi-head self-attention within each text:
+ * out[rows of text i, head h] = softmax(Q_h K_h^T / sqrt(d_head)) V_h.
+ * d_qkv bf16 [T, 3 n_heads d_head] (Q | K | V blocks, head h at columns
+ * h d_head of each); d_out bf16 [T, n_heads d_head]; T = cu[n_texts].
+ * d_head is 32 or 64; n_heads * d_head % 128 == 0.
+ */
+surge_status surge_op_attention(int64_t n_texts, const int64_t* h_cu_seqlens, int32_t n_heads,
+                                int32_t d_head, const uint16_t* d_qkv, uint16_t* d_out,
+                                void* hip_stream);
+
+/* Row LayerNorm: y = gamma (x - mean) / sqrt(var + eps) + beta, biased
+ * variance.  d_x, d_y bf16 [M, d]; d % 8 == 0, d <= 1024. */
+surge_status surge_op_layernorm(int64_t M, int32_t d, const uint16_t* d_x, const float* d_gamma,
+                                const float* d_beta, float eps, uint16_t* d_y, void* hip_stream);
+
+/* Masked mean pooling + L2 normalisation: out[i] = e_i / max(||e_i||, 1e-12)
+ * with e_i the mean of text i's rows of d_x (bf16 [T, d]); d_out fp32
+ * [n_texts, d], 16-byte aligned.  d % 128 == 0, d <= 1024. */
+surge_status surge_op_pool_l2(int64_t n_texts, const int64_t* h_cu_seqlens, int32_t d,
+                              const uint16_t* d_x, float* d_out, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SURGE_OPS_H_ */

@@ -1,0 +1,543 @@
+// The encoder object and the SuperBatch encode path.
+//
+// Create: validate the description, round matrices and embedding tables to
+// bf16, transpose every matrix to [out, in] (K-contiguous for the MFMA
+// linear kernel) and upload everything in one device block; allocate the
+// activation workspace for max_tokens_per_chunk tokens.
+//
+// Encode one SuperBatch (Alg. 1, Flush): validate on the host, resolve every
+// text's output row pointer from the segment table, cut the SuperBatch into
+// token chunks at text boundaries, and for each chunk upload (cu_seqlens,
+// row pointers) through a pinned staging ring and launch
+//   embed+LN, then per layer: QKV, attention, O-proj+residual, LN1,
+//   FFN1+GELU, FFN2+residual, LN2, and finally pool+L2+scatter.
+// Everything is enqueued on the caller's stream; nothing blocks except the
+// reuse of a staging slot whose previous copy is still pending.
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "internal.h"
+#include "kernels.h"
+
+using namespace surge;
+
+namespace {
+
+constexpr int kStagingSlots = 4;
+
+struct LayerWeights {
+  uint16_t *wqkv, *wo, *w1, *w2;               // bf16 [out, in]
+  float *bqkv, *bo, *ln1g, *ln1b, *b1, *b2, *ln2g, *ln2b;  // fp32
+};
+
+struct ProfRecord {
+  int kind;
+  int ev;  // index of the start event; stop is ev + 1
+  double flops, bytes;
+};
+
+}  // namespace
+
+struct surge_encoder {
+  surge_encoder_desc desc;
+  int device = 0;
+  int64_t max_tokens = 0;
+  // weights
+  void* wblock = nullptr;
+  uint16_t *word = nullptr, *pos = nullptr;
+  float *lneg = nullptr, *lneb = nullptr;
+  std::vector<LayerWeights> layers;
+  // workspace
+  void* wsblock = nullptr;
+  int64_t ws_bytes = 0;
+  uint16_t *X = nullptr, *QKV = nullptr, *CTX = nullptr, *Y = nullptr, *H = nullptr;
+  int32_t* d_cu = nullptr;     // [max_tokens + 1]
+  uint64_t* d_dst = nullptr;   // [max_tokens]
+  int* d_err = nullptr;
+  // pinned staging ring for chunk metadata
+  void* staging[kStagingSlots] = {};
+  hipEvent_t staging_ev[kStagingSlots] = {};
+  bool staging_used[kStagingSlots] = {};
+  int staging_next = 0;
+  size_t staging_bytes = 0;
+  // host scratch
+  std::vector<uint64_t> h_dst;
+  // profiling
+  bool prof = false;
+  std::vector<hipEvent_t> prof_events;
+  int prof_used = 0;
+  std::vector<ProfRecord> prof_recs;
+};
+
+#define HIP_TRY(expr)                                                                    \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess)                                                                \
+      return fail(e_ == hipErrorOutOfMemory ? SURGE_ERR_OUT_OF_MEMORY : SURGE_ERR_DEVICE, \
+                  "%s failed: %s", #expr, hipGetErrorString(e_));                        \
+  } while (0)
+
+namespace {
+
+void free_encoder(surge_encoder* e) {
+  if (!e) return;
+  hipSetDevice(e->device);
+  hipDeviceSynchronize();
+  for (int i = 0; i < kStagingSlots; ++i) {
+    if (e->staging_ev[i]) hipEventDestroy(e->staging_ev[i]);
+    if (e->staging[i]) hipHostFree(e->staging[i]);
+  }
+  for (hipEvent_t ev : e->prof_events) hipEventDestroy(ev);
+  if (e->wblock) hipFree(e->wblock);
+  if (e->wsblock) hipFree(e->wsblock);
+  delete e;
+}
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Profiling: start/stop event pair around one launch.
+surge_status prof_begin(surge_encoder* e, hipStream_t s, int* ev) {
+  if (!e->prof) return SURGE_OK;
+  if ((size_t)e->prof_used + 2 > e->prof_events.size()) {
+    for (int i = 0; i < 256; ++i) {
+      hipEvent_t x;
+      HIP_TRY(hipEventCreate(&x));
+      e->prof_events.push_back(x);
+    }
+  }
+  *ev = e->prof_used;
+  e->prof_used += 2;
+  HIP_TRY(hipEventRecord(e->prof_events[*ev], s));
+  return SURGE_OK;
+}
+
+surge_status prof_end(surge_encoder* e, hipStream_t s, int ev, int kind, double flops,
+                      double bytes) {
+  if (!e->prof) return SURGE_OK;
+  HIP_TRY(hipEventRecord(e->prof_events[ev + 1], s));
+  e->prof_recs.push_back(ProfRecord{kind, ev, flops, bytes});
+  return SURGE_OK;
+}
+
+#define LAUNCH(kind, flops, bytes, call)                             \
+  do {                                                               \
+    int ev_ = -1;                                                    \
+    surge_status st_ = prof_begin(e, stream, &ev_);                  \
+    if (st_ != SURGE_OK) return st_;                                 \
+    hipError_t le_ = (call);                                         \
+    if (le_ != hipSuccess)                                           \
+      return fail(SURGE_ERR_DEVICE, "kernel launch failed: %s", hipGetErrorString(le_)); \
+    st_ = prof_end(e, stream, ev_, kind, flops, bytes);              \
+    if (st_ != SURGE_OK) return st_;                                 \
+  } while (0)
+
+// Encode texts [0, n_texts) of a validated SuperBatch whose row pointers are
+// in e->h_dst.  cu is SuperBatch-local host int64.
+surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_tokens,
+                           const int64_t* cu, hipStream_t stream) {
+  const surge_encoder_desc& D = e->desc;
+  const int d = D.d_model, f = D.d_ff, dh = d / D.n_heads;
+  int64_t t0 = 0;
+  while (t0 < n_texts) {
+    // Largest run of whole texts that fits the workspace.
+    int64_t t1 = t0;
+    while (t1 < n_texts && cu[t1 + 1] - cu[t0] <= e->max_tokens) ++t1;
+    const int64_t S = t1 - t0;
+    const int64_t T = cu[t1] - cu[t0];
+
+    // Stage (cu32 [S+1], dst [S]) in a pinned slot, then copy to the device.
+    const int slot = e->staging_next;
+    e->staging_next = (slot + 1) % kStagingSlots;
+    if (e->staging_used[slot]) HIP_TRY(hipEventSynchronize(e->staging_ev[slot]));
+    const size_t cu_bytes = align_up((size_t)(S + 1) * 4, 16);
+    int32_t* hcu = (int32_t*)e->staging[slot];
+    uint64_t* hdst = (uint64_t*)((char*)e->staging[slot] + align_up((size_t)(e->max_tokens + 1) * 4, 16));
+    for (int64_t i = 0; i <= S; ++i) hcu[i] = (int32_t)(cu[t0 + i] - cu[t0]);
+    memcpy(hdst, e->h_dst.data() + t0, (size_t)S * 8);
+    HIP_TRY(hipMemcpyAsync(e->d_cu, hcu, cu_bytes, hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipMemcpyAsync(e->d_dst, hdst, (size_t)S * 8, hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipEventRecord(e->staging_ev[slot], stream));
+    e->staging_used[slot] = true;
+
+    const int32_t* toks = d_tokens + cu[t0];
+    double sumL2 = 0.0;
+    for (int64_t i = t0; i < t1; ++i) {
+      const double L = (double)(cu[i + 1] - cu[i]);
+      sumL2 += L * L;
+    }
+    const double Td = (double)T;
+    const int Si = (int)S;
+
+    LAUNCH(SURGE_KERNEL_EMBED, 0.0, Td * (4.0 + 6.0 * d),
+           launch_embed_ln(toks, e->d_cu, Si, e->word, e->pos, e->lneg, e->lneb, D.ln_eps,
+                           D.vocab_size, d, e->X, e->d_err, stream));
+    for (int l = 0; l < D.n_layers; ++l) {
+      const LayerWeights& w = e->layers[l];
+      LAUNCH(SURGE_KERNEL_QKV, 2.0 * Td * d * 3 * d, 2.0 * (Td * d + 3.0 * d * d + Td * 3 * d),
+             launch_linear(e->X, w.wqkv, w.bqkv, nullptr, e->QKV, T, 3 * d, d, EPI_BIAS, stream));
+      LAUNCH(SURGE_KERNEL_ATTN, 4.0 * d * sumL2, 2.0 * Td * 4 * d,
+             launch_attention(e->QKV, e->CTX, e->d_cu, Si, D.n_heads, dh, stream));
+      LAUNCH(SURGE_KERNEL_OPROJ, 2.0 * Td * d * d, 2.0 * (3.0 * Td * d + (double)d * d),
+             launch_linear(e->CTX, w.wo, w.bo, e->X, e->Y, T, d, d, EPI_BIAS_RESIDUAL, stream));
+      LAUNCH(SURGE_KERNEL_LN1, 0.0, 4.0 * Td * d,
+             launch_layernorm(e->Y, w.ln1g, w.ln1b, D.ln_eps, e->X, T, d, stream));
+      LAUNCH(SURGE_KERNEL_FFN1, 2.0 * Td * d * f, 2.0 * (Td * d + (double)d * f + Td * f),
+             launch_linear(e->X, w.w1, w.b1, nullptr, e->H, T, f, d, EPI_BIAS_GELU, stream));
+      LAUNCH(SURGE_KERNEL_FFN2, 2.0 * Td * d * f, 2.0 * (Td * f + (double)d * f + 2.0 * Td * d),
+             launch_linear(e->H, w.w2, w.b2, e->X, e->Y, T, d, f, EPI_BIAS_RESIDUAL, stream));
+      LAUNCH(SURGE_KERNEL_LN2, 0.0, 4.0 * Td * d,
+             launch_layernorm(e->Y, w.ln2g, w.ln2b, D.ln_eps, e->X, T, d, stream));
+    }
+    LAUNCH(SURGE_KERNEL_POOL, 0.0, 2.0 * Td * d + 4.0 * S * d,
+           launch_pool_l2_scatter(e->X, e->d_cu, Si, e->d_dst, d, stream));
+    t0 = t1;
+  }
+  return SURGE_OK;
+}
+
+// Resolve text -> output row pointer from a validated segment table.
+void resolve_rows(surge_encoder* e, int64_t n_texts, const surge_segment* segs, int64_t n_segs,
+                  float* const* part_out) {
+  e->h_dst.resize((size_t)n_texts);
+  const int64_t d = e->desc.d_model;
+  for (int64_t s = 0; s < n_segs; ++s) {
+    const surge_segment& g = segs[s];
+    float* base = part_out[g.partition] + g.row_offset * d;
+    for (int64_t k = 0; k < g.count; ++k)
+      e->h_dst[(size_t)(g.first_text + k)] = (uint64_t)(uintptr_t)(base + k * d);
+  }
+}
+
+surge_status check_alignment(int64_t n_segs, const surge_segment* segs, float* const* part_out) {
+  for (int64_t s = 0; s < n_segs; ++s)
+    if (((uintptr_t)part_out[segs[s].partition]) & 15u)
+      return fail(SURGE_ERR_INVALID_ARGUMENT, "output of partition %d is not 16-byte aligned",
+                  segs[s].partition);
+  return SURGE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* const* host_weights,
+                                  int32_t n_weights, int64_t max_tokens_per_chunk,
+                                  surge_encoder** out) {
+  clear_error();
+  if (!out) return fail(SURGE_ERR_INVALID_ARGUMENT, "out is NULL");
+  *out = nullptr;
+  surge_status st = validate_desc(desc);
+  if (st != SURGE_OK) return st;
+  const surge_encoder_desc D = *desc;
+  const int64_t expect = 4 + 12 * (int64_t)D.n_layers;
+  if (!host_weights || n_weights != expect)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "expected %lld weight arrays, got %d",
+                (long long)expect, n_weights);
+  for (int i = 0; i < n_weights; ++i)
+    if (!host_weights[i]) return fail(SURGE_ERR_INVALID_ARGUMENT, "weight %d is NULL", i);
+  if (max_tokens_per_chunk < D.max_positions || max_tokens_per_chunk > (int64_t)1 << 30)
+    return fail(SURGE_ERR_INVALID_ARGUMENT,
+                "max_tokens_per_chunk=%lld outside [max_positions, 2^30]",
+                (long long)max_tokens_per_chunk);
+
+  surge_encoder* e = new surge_encoder();
+  e->desc = D;
+  e->max_tokens = max_tokens_per_chunk;
+  hipError_t he = hipGetDevice(&e->device);
+  if (he != hipSuccess) {
+    delete e;
+    return fail(SURGE_ERR_DEVICE, "hipGetDevice failed: %s", hipGetErrorString(he));
+  }
+
+  const int64_t d = D.d_model, f = D.d_ff, V = D.vocab_size, P = D.max_positions;
+  // Device weight block layout (byte offsets, 256-aligned pieces).
+  std::vector<size_t> offs;
+  size_t total = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = total;
+    total = align_up(total + bytes, 256);
+    offs.push_back(o);
+    return o;
+  };
+  take((size_t)V * d * 2);  // word
+  take((size_t)P * d * 2);  // pos
+  take((size_t)d * 4);      // ln_e gamma
+  take((size_t)d * 4);      // ln_e beta
+  const int64_t mshape[4][2] = {{d, 3 * d}, {d, d}, {d, f}, {f, d}};  // [in, out]
+  for (int l = 0; l < D.n_layers; ++l) {
+    take((size_t)d * 3 * d * 2);  // wqkv
+    take((size_t)3 * d * 4);      // bqkv
+    take((size_t)d * d * 2);      // wo
+    take((size_t)d * 4);          // bo
+    take((size_t)d * 4);          // ln1g
+    take((size_t)d * 4);          // ln1b
+    take((size_t)d * f * 2);      // w1
+    take((size_t)f * 4);          // b1
+    take((size_t)f * d * 2);      // w2
+    take((size_t)d * 4);          // b2
+    take((size_t)d * 4);          // ln2g
+    take((size_t)d * 4);          // ln2b
+  }
+  (void)mshape;
+  std::vector<uint8_t> host(total, 0);
+  auto put_bf16 = [&](int idx, const float* src, int64_t n) {
+    uint16_t* dst = (uint16_t*)(host.data() + offs[idx]);
+    for (int64_t i = 0; i < n; ++i) dst[i] = f32_to_bf16_rne(src[i]);
+  };
+  auto put_bf16_t = [&](int idx, const float* src, int64_t in, int64_t outn) {
+    // src [in, out] row-major -> dst [out, in]
+    uint16_t* dst = (uint16_t*)(host.data() + offs[idx]);
+    for (int64_t i = 0; i < in; ++i)
+      for (int64_t o = 0; o < outn; ++o) dst[o * in + i] = f32_to_bf16_rne(src[i * outn + o]);
+  };
+  auto put_f32 = [&](int idx, const float* src, int64_t n) {
+    memcpy(host.data() + offs[idx], src, (size_t)n * 4);
+  };
+  put_bf16(0, host_weights[0], V * d);
+  put_bf16(1, host_weights[1], P * d);
+  put_f32(2, host_weights[2], d);
+  put_f32(3, host_weights[3], d);
+  for (int l = 0; l < D.n_layers; ++l) {
+    const int b = 4 + 12 * l;
+    put_bf16_t(b + 0, host_weights[b + 0], d, 3 * d);
+    put_f32(b + 1, host_weights[b + 1], 3 * d);
+    put_bf16_t(b + 2, host_weights[b + 2], d, d);
+    put_f32(b + 3, host_weights[b + 3], d);
+    put_f32(b + 4, host_weights[b + 4], d);
+    put_f32(b + 5, host_weights[b + 5], d);
+    put_bf16_t(b + 6, host_weights[b + 6], d, f);
+    put_f32(b + 7, host_weights[b + 7], f);
+    put_bf16_t(b + 8, host_weights[b + 8], f, d);
+    put_f32(b + 9, host_weights[b + 9], d);
+    put_f32(b + 10, host_weights[b + 10], d);
+    put_f32(b + 11, host_weights[b + 11], d);
+  }
+
+  auto cleanup_fail = [&](surge_status code) {
+    free_encoder(e);
+    return code;
+  };
+  hipError_t err = hipMalloc(&e->wblock, total);
+  if (err != hipSuccess)
+    return cleanup_fail(fail(SURGE_ERR_OUT_OF_MEMORY, "weights: hipMalloc(%zu) failed: %s", total,
+                             hipGetErrorString(err)));
+  err = hipMemcpy(e->wblock, host.data(), total, hipMemcpyHostToDevice);
+  if (err != hipSuccess)
+    return cleanup_fail(fail(SURGE_ERR_DEVICE, "weights: hipMemcpy failed: %s", hipGetErrorString(err)));
+  char* wb = (char*)e->wblock;
+  e->word = (uint16_t*)(wb + offs[0]);
+  e->pos = (uint16_t*)(wb + offs[1]);
+  e->lneg = (float*)(wb + offs[2]);
+  e->lneb = (float*)(wb + offs[3]);
+  for (int l = 0; l < D.n_layers; ++l) {
+    const int b = 4 + 12 * l;
+    LayerWeights w;
+    w.wqkv = (uint16_t*)(wb + offs[b + 0]);
+    w.bqkv = (float*)(wb + offs[b + 1]);
+    w.wo = (uint16_t*)(wb + offs[b + 2]);
+    w.bo = (float*)(wb + offs[b + 3]);
+    w.ln1g = (float*)(wb + offs[b + 4]);
+    w.ln1b = (float*)(wb + offs[b + 5]);
+    w.w1 = (uint16_t*)(wb + offs[b + 6]);
+    w.b1 = (float*)(wb + offs[b + 7]);
+    w.w2 = (uint16_t*)(wb + offs[b + 8]);
+    w.b2 = (float*)(wb + offs[b + 9]);
+    w.ln2g = (float*)(wb + offs[b + 10]);
+    w.ln2b = (float*)(wb + offs[b + 11]);
+    e->layers.push_back(w);
+  }
+
+  // Workspace: X, QKV, CTX, Y, H activations + metadata + error flag.
+  const int64_t T = max_tokens_per_chunk;
+  size_t ws = 0;
+  std::vector<size_t> wo;
+  auto wtake = [&](size_t bytes) {
+    size_t o = ws;
+    ws = align_up(ws + bytes, 256);
+    wo.push_back(o);
+  };
+  wtake((size_t)T * d * 2);        // X
+  wtake((size_t)T * 3 * d * 2);    // QKV
+  wtake((size_t)T * d * 2);        // CTX
+  wtake((size_t)T * d * 2);        // Y
+  wtake((size_t)T * f * 2);        // H
+  wtake((size_t)(T + 1) * 4 + 16); // cu
+  wtake((size_t)T * 8);            // dst
+  wtake(256);                      // err
+  err = hipMalloc(&e->wsblock, ws);
+  if (err != hipSuccess)
+    return cleanup_fail(fail(SURGE_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed: %s", ws,
+                             hipGetErrorString(err)));
+  e->ws_bytes = (int64_t)ws;
+  char* w = (char*)e->wsblock;
+  e->X = (uint16_t*)(w + wo[0]);
+  e->QKV = (uint16_t*)(w + wo[1]);
+  e->CTX = (uint16_t*)(w + wo[2]);
+  e->Y = (uint16_t*)(w + wo[3]);
+  e->H = (uint16_t*)(w + wo[4]);
+  e->d_cu = (int32_t*)(w + wo[5]);
+  e->d_dst = (uint64_t*)(w + wo[6]);
+  e->d_err = (int*)(w + wo[7]);
+  err = hipMemset(e->d_err, 0, 256);
+  if (err != hipSuccess)
+    return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipMemset failed: %s", hipGetErrorString(err)));
+
+  e->staging_bytes = align_up((size_t)(T + 1) * 4, 16) + (size_t)T * 8;
+  for (int i = 0; i < kStagingSlots; ++i) {
+    err = hipHostMalloc(&e->staging[i], e->staging_bytes, hipHostMallocDefault);
+    if (err != hipSuccess)
+      return cleanup_fail(fail(SURGE_ERR_OUT_OF_MEMORY, "hipHostMalloc failed: %s",
+                               hipGetErrorString(err)));
+    err = hipEventCreateWithFlags(&e->staging_ev[i], hipEventDisableTiming);
+    if (err != hipSuccess)
+      return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipEventCreate failed: %s", hipGetErrorString(err)));
+  }
+  *out = e;
+  return SURGE_OK;
+}
+
+void surge_encoder_destroy(surge_encoder* enc) { free_encoder(enc); }
+
+surge_status surge_encoder_info(const surge_encoder* enc, surge_encoder_desc* desc,
+                                int64_t* max_tokens_per_chunk, int64_t* workspace_bytes) {
+  clear_error();
+  if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
+  if (desc) *desc = enc->desc;
+  if (max_tokens_per_chunk) *max_tokens_per_chunk = enc->max_tokens;
+  if (workspace_bytes) *workspace_bytes = enc->ws_bytes;
+  return SURGE_OK;
+}
+
+surge_status surge_encode_superbatch(surge_encoder* enc, int64_t n_texts, int64_t n_tokens,
+                                     const int32_t* d_token_ids, const int64_t* h_cu_seqlens,
+                                     const surge_segment* h_segs, int64_t n_segs,
+                                     float* const* h_part_out, const int64_t* h_part_sizes,
+                                     int32_t n_parts, void* hip_stream) {
+  clear_error();
+  if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
+  surge_status st = surge_validate_superbatch(&enc->desc, n_texts, n_tokens, h_cu_seqlens, h_segs,
+                                              n_segs, h_part_sizes, h_part_out, n_parts);
+  if (st != SURGE_OK) return st;
+  if (n_texts > 0 && !d_token_ids) return fail(SURGE_ERR_INVALID_ARGUMENT, "token_ids is NULL");
+  st = check_alignment(n_segs, h_segs, h_part_out);
+  if (st != SURGE_OK) return st;
+  if (n_texts == 0) return SURGE_OK;
+  HIP_TRY(hipSetDevice(enc->device));
+  surge_encoder* e = enc;
+  resolve_rows(e, n_texts, h_segs, n_segs, h_part_out);
+  return encode_chunks(e, n_texts, d_token_ids, h_cu_seqlens, (hipStream_t)hip_stream);
+}
+
+surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t* d_token_ids,
+                              const int64_t* h_cu_seqlens, const int64_t* h_part_offsets,
+                              int32_t n_parts, int64_t b_min, int64_t n_max, int32_t policy,
+                              float* const* h_part_out, int64_t first_sb, int64_t* n_superbatches,
+                              void* hip_stream) {
+  clear_error();
+  if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
+  if (!h_part_offsets || !h_cu_seqlens || !h_part_out)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL host array");
+  if (n_parts < 0 || h_part_offsets[n_parts] != n_texts)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts] != n_texts");
+  if (first_sb < 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "first_sb < 0");
+  struct Ctx {
+    std::vector<PlanSB> sbs;
+    std::vector<surge_segment> segs;
+  } ctx;
+  auto on_sb = [](void* c, const PlanSB& s) { ((Ctx*)c)->sbs.push_back(s); };
+  auto on_seg = [](void* c, const PlanSeg& s) {
+    surge_segment g;
+    g.first_text = s.first_text;
+    g.count = s.count;
+    g.row_offset = s.row_offset;
+    g.partition = s.partition;
+    g.reserved = 0;
+    ((Ctx*)c)->segs.push_back(g);
+  };
+  int64_t ns = 0, ng = 0;
+  surge_status st = plan_superbatches(h_part_offsets, n_parts, b_min, n_max, policy, on_sb, on_seg,
+                                      &ctx, &ns, &ng);
+  if (st != SURGE_OK) return st;
+  if (n_superbatches) *n_superbatches = ns;
+  // Validate the whole input once, then every SuperBatch is consistent.
+  std::vector<int64_t> sizes((size_t)n_parts);
+  for (int32_t p = 0; p < n_parts; ++p) sizes[p] = h_part_offsets[p + 1] - h_part_offsets[p];
+  st = surge_validate_superbatch(&enc->desc, n_texts, h_cu_seqlens[n_texts], h_cu_seqlens,
+                                 ctx.segs.data(), (int64_t)ctx.segs.size(), sizes.data(),
+                                 h_part_out, n_parts);
+  if (st != SURGE_OK) return st;
+  st = check_alignment((int64_t)ctx.segs.size(), ctx.segs.data(), h_part_out);
+  if (st != SURGE_OK) return st;
+  if (n_texts > 0 && !d_token_ids) return fail(SURGE_ERR_INVALID_ARGUMENT, "token_ids is NULL");
+  if (n_texts == 0) return SURGE_OK;
+  HIP_TRY(hipSetDevice(enc->device));
+  surge_encoder* e = enc;
+  std::vector<int64_t> lcu;
+  for (int64_t k = first_sb; k < ns; ++k) {
+    const PlanSB& sb = ctx.sbs[(size_t)k];
+    const int64_t S = sb.text_end - sb.text_begin;
+    lcu.resize((size_t)S + 1);
+    const int64_t base = h_cu_seqlens[sb.text_begin];
+    for (int64_t i = 0; i <= S; ++i) lcu[(size_t)i] = h_cu_seqlens[sb.text_begin + i] - base;
+    // Row pointers of the SuperBatch's texts (segments are global here).
+    e->h_dst.resize((size_t)S);
+    const int64_t d = e->desc.d_model;
+    for (int64_t s = sb.seg_begin; s < sb.seg_end; ++s) {
+      const surge_segment& g = ctx.segs[(size_t)s];
+      float* rb = h_part_out[g.partition] + g.row_offset * d;
+      for (int64_t j = 0; j < g.count; ++j)
+        e->h_dst[(size_t)(g.first_text - sb.text_begin + j)] = (uint64_t)(uintptr_t)(rb + j * d);
+    }
+    st = encode_chunks(e, S, d_token_ids + base, lcu.data(), (hipStream_t)hip_stream);
+    if (st != SURGE_OK) return st;
+  }
+  return SURGE_OK;
+}
+
+surge_status surge_check(surge_encoder* enc, void* hip_stream) {
+  clear_error();
+  if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
+  HIP_TRY(hipSetDevice(enc->device));
+  HIP_TRY(hipStreamSynchronize((hipStream_t)hip_stream));
+  int flag = 0;
+  HIP_TRY(hipMemcpy(&flag, enc->d_err, sizeof(int), hipMemcpyDeviceToHost));
+  if (flag) {
+    HIP_TRY(hipMemset(enc->d_err, 0, sizeof(int)));
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "a token ID outside [0, vocab) was encoded as ID 0");
+  }
+  return SURGE_OK;
+}
+
+surge_status surge_profile_enable(surge_encoder* enc, int32_t on) {
+  clear_error();
+  if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
+  enc->prof = on != 0;
+  enc->prof_used = 0;
+  enc->prof_recs.clear();
+  return SURGE_OK;
+}
+
+surge_status surge_profile_read(surge_encoder* enc, surge_kernel_stat* stats, int32_t n_stats) {
+  clear_error();
+  if (!enc || !stats) return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL argument");
+  for (int i = 0; i < n_stats; ++i) stats[i] = surge_kernel_stat{0, 0.0, 0.0, 0.0};
+  HIP_TRY(hipSetDevice(enc->device));
+  for (const ProfRecord& r : enc->prof_recs) {
+    if (r.kind >= n_stats) continue;
+    HIP_TRY(hipEventSynchronize(enc->prof_events[r.ev + 1]));
+    float ms = 0.0f;
+    HIP_TRY(hipEventElapsedTime(&ms, enc->prof_events[r.ev], enc->prof_events[r.ev + 1]));
+    surge_kernel_stat& s = stats[r.kind];
+    s.launches += 1;
+    s.total_ms += ms;
+    s.flops += r.flops;
+    s.bytes += r.bytes;
+  }
+  return SURGE_OK;
+}
+
+}  // extern "C"

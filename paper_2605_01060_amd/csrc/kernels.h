@@ -1,0 +1,41 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher assumes its
+// arguments were checked by the caller (shapes, alignment, index ranges) and
+// returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace surge {
+
+// x_t = LN(word[id_t] + pos[t - cu_i]) for every token of n_texts texts.
+// tokens [cu[n_texts]], cu int32 [n_texts+1] (device), out bf16 [T, d].
+// Out-of-vocabulary IDs are gathered as ID 0 and set *err = 1.
+hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts,
+                           const uint16_t* word, const uint16_t* pos, const float* gamma,
+                           const float* beta, float eps, int vocab, int d, uint16_t* out, int* err,
+                           hipStream_t stream);
+
+// Y[M, N] = epi(X[M, K] W^T + b), W stored [N, K] (out, in), bf16 in/out.
+// epi: 0 = bias, 1 = bias then GELU, 2 = bias then + R[M, N].
+// Requires N % 128 == 0, K % 64 == 0, M >= 1.
+enum LinearEpilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESIDUAL = 2 };
+hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
+                         uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream);
+
+// Packed varlen multi-head self-attention.  qkv bf16 [T, 3 H dh] (Q | K | V
+// column blocks, head h at columns h*dh of each), out bf16 [T, H dh].
+// Attention runs within each text only.  dh is 32 or 64.
+hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* cu, int n_texts,
+                            int n_heads, int d_head, hipStream_t stream);
+
+// y = LN(x) per row of d (d % 8 == 0, d <= 1024), bf16 in/out.
+hipError_t launch_layernorm(const uint16_t* x, const float* gamma, const float* beta, float eps,
+                            uint16_t* y, int64_t M, int d, hipStream_t stream);
+
+// e_i = mean of text i's rows of x; row i of the output (dst[i], a device
+// pointer to d floats) = e_i / max(||e_i||, 1e-12).
+hipError_t launch_pool_l2_scatter(const uint16_t* x, const int32_t* cu, int n_texts,
+                                  const uint64_t* dst, int d, hipStream_t stream);
+
+}  // namespace surge

@@ -1,0 +1,197 @@
+// Row-wise, HBM-bound kernels: embedding gather + LayerNorm, LayerNorm, and
+// masked mean pooling + L2 normalisation + partition scatter.
+//
+// A row of d bf16 values is read as d/8 16-byte chunks spread over the 64
+// lanes of one wave (at most two chunks per lane for d <= 1024); mean and
+// variance are wave reductions in fp32 (two passes over the registers, so
+// the variance is taken about the mean).
+#include <math.h>
+
+#include "device_common.h"
+#include "kernels.h"
+
+namespace surge {
+namespace {
+
+constexpr int MAXC = 2;  // 16-byte chunks per lane, d <= 64 * 2 * 8 = 1024
+
+__device__ __forceinline__ void ln_row(float (&v)[MAXC][8], int nch, int lane, int d,
+                                       const float* __restrict__ gamma,
+                                       const float* __restrict__ beta, float eps,
+                                       uint16_t* __restrict__ yrow) {
+  float s = 0.0f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    if (lane + 64 * c < nch) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[c][e];
+    }
+  }
+  const float mean = wave_sum(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    if (lane + 64 * c < nch) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float t = v[c][e] - mean;
+        q += t * t;
+      }
+    }
+  }
+  const float var = wave_sum(q) / (float)d;
+  const float rstd = 1.0f / sqrtf(var + eps);
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int ch = lane + 64 * c;
+    if (ch < nch) {
+      const float4 g0 = reinterpret_cast<const float4*>(gamma)[2 * ch];
+      const float4 g1 = reinterpret_cast<const float4*>(gamma)[2 * ch + 1];
+      const float4 b0 = reinterpret_cast<const float4*>(beta)[2 * ch];
+      const float4 b1 = reinterpret_cast<const float4*>(beta)[2 * ch + 1];
+      const float g[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+      const float b[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+      float o[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (v[c][e] - mean) * rstd * g[e] + b[e];
+      reinterpret_cast<uint4*>(yrow)[ch] = pack8(o);
+    }
+  }
+}
+
+// One block per text; its four waves take the text's tokens in turn.
+__global__ __launch_bounds__(256) void embed_ln_kernel(
+    const int32_t* __restrict__ tokens, const int32_t* __restrict__ cu,
+    const uint16_t* __restrict__ word, const uint16_t* __restrict__ pos,
+    const float* __restrict__ gamma, const float* __restrict__ beta, float eps, int vocab, int d,
+    uint16_t* __restrict__ out, int* __restrict__ err) {
+  const int t = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int beg = cu[t];
+  const int L = cu[t + 1] - beg;
+  const int nch = d >> 3;
+  for (int p = wave; p < L; p += 4) {
+    int id = tokens[beg + p];
+    if (id < 0 || id >= vocab) {
+      if (lane == 0) atomicOr(err, 1);
+      id = 0;
+    }
+    const uint4* wr = reinterpret_cast<const uint4*>(word + (size_t)id * d);
+    const uint4* pr = reinterpret_cast<const uint4*>(pos + (size_t)p * d);
+    float v[MAXC][8];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      const int ch = lane + 64 * c;
+      if (ch < nch) {
+        float a[8], b[8];
+        unpack8(wr[ch], a);
+        unpack8(pr[ch], b);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[c][e] = a[e] + b[e];
+      }
+    }
+    ln_row(v, nch, lane, d, gamma, beta, eps, out + (size_t)(beg + p) * d);
+  }
+}
+
+// One wave per row, four rows per block.
+__global__ __launch_bounds__(256) void layernorm_kernel(const uint16_t* __restrict__ x,
+                                                        const float* __restrict__ gamma,
+                                                        const float* __restrict__ beta, float eps,
+                                                        uint16_t* __restrict__ y, int64_t M,
+                                                        int d) {
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= M) return;
+  const int nch = d >> 3;
+  const uint4* xr = reinterpret_cast<const uint4*>(x + (size_t)row * d);
+  float v[MAXC][8];
+#pragma unroll
+  for (int c = 0; c < MAXC; ++c) {
+    const int ch = lane + 64 * c;
+    if (ch < nch) unpack8(xr[ch], v[c]);
+  }
+  ln_row(v, nch, lane, d, gamma, beta, eps, y + (size_t)row * d);
+}
+
+// One block per text: 2 groups of 128 threads split the text's rows, each
+// thread owns one 16-byte column chunk; the norm is a block reduction.
+__global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __restrict__ x,
+                                                              const int32_t* __restrict__ cu,
+                                                              const uint64_t* __restrict__ dst,
+                                                              int d) {
+  __shared__ float part[128 * 8];
+  __shared__ float red[4];
+  const int t = blockIdx.x;
+  const int c = threadIdx.x & 127;
+  const int grp = threadIdx.x >> 7;
+  const int beg = cu[t];
+  const int L = cu[t + 1] - beg;
+  const int nch = d >> 3;
+  float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (c < nch) {
+    for (int p = grp; p < L; p += 2) {
+      float f[8];
+      unpack8(reinterpret_cast<const uint4*>(x + (size_t)(beg + p) * d)[c], f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += f[e];
+    }
+  }
+  if (grp == 1 && c < nch) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[c * 8 + e] = acc[e];
+  }
+  __syncthreads();
+  float sq = 0.0f;
+  if (grp == 0 && c < nch) {
+    const float invL = 1.0f / (float)L;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[e] = (acc[e] + part[c * 8 + e]) * invL;
+      sq += acc[e] * acc[e];
+    }
+  }
+  sq = wave_sum(sq);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sq;
+  __syncthreads();
+  const float norm = sqrtf(red[0] + red[1]);
+  const float inv = 1.0f / fmaxf(norm, 1e-12f);
+  if (grp == 0 && c < nch) {
+    float* row = reinterpret_cast<float*>(dst[t]);
+    float4 a = make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    float4 b = make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv);
+    reinterpret_cast<float4*>(row)[2 * c] = a;
+    reinterpret_cast<float4*>(row)[2 * c + 1] = b;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts,
+                           const uint16_t* word, const uint16_t* pos, const float* gamma,
+                           const float* beta, float eps, int vocab, int d, uint16_t* out, int* err,
+                           hipStream_t stream) {
+  if (n_texts <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_ln_kernel, dim3(n_texts), dim3(256), 0, stream, tokens, cu, word, pos,
+                     gamma, beta, eps, vocab, d, out, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_layernorm(const uint16_t* x, const float* gamma, const float* beta, float eps,
+                            uint16_t* y, int64_t M, int d, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)((M + 3) / 4);
+  hipLaunchKernelGGL(layernorm_kernel, dim3(blocks), dim3(256), 0, stream, x, gamma, beta, eps, y,
+                     M, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_l2_scatter(const uint16_t* x, const int32_t* cu, int n_texts,
+                                  const uint64_t* dst, int d, hipStream_t stream) {
+  if (n_texts <= 0) return hipSuccess;
+  hipLaunchKernelGGL(pool_l2_scatter_kernel, dim3(n_texts), dim3(256), 0, stream, x, cu, dst, d);
+  return hipGetLastError();
+}
+
+}  // namespace surge

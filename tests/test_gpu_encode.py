@@ -1,0 +1,212 @@
+"""End-to-end parity of SuperBatch encoding through the C-ABI.
+
+Every configuration runs the whole workload through surge_encode_all (the
+call the benchmark times); the tiny one is compared on every text, the full
+sized ones on a sample that covers the first and last text of SuperBatches
+and the rows around every split-partition boundary.  Outputs are NaN-filled
+before the call, so a row never written (or written to the wrong place)
+shows up.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import assert_parity, desc_of, torch_cuda, weight_list
+from oracle import encoder as E
+from oracle import plan as OP
+from paper_2605_01060_amd import surge as S
+from paper_2605_01060_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+
+_cache = {}
+
+
+def _setup(name):
+    if name not in _cache:
+        spec = W.WORKLOADS[name]
+        wl = W.make_workload(spec)
+        weights = W.make_weights(spec.encoder, seed=spec.seed)
+        _cache.clear()
+        _cache[name] = (spec, wl, weights)
+    return _cache[name]
+
+
+def _outputs(torch, wl, d):
+    out = torch.full((wl.n_texts, d), float("nan"), device="cuda")
+    ptrs = np.array([out.data_ptr() + int(o) * d * 4 for o in wl.part_offsets[:-1]],
+                    dtype=np.uint64)
+    return out, ptrs
+
+
+def _encode_all(torch, enc, wl, d, b_min, n_max, policy=S.SURGE_POLICY_SPLIT):
+    out, ptrs = _outputs(torch, wl, d)
+    tok = torch.from_numpy(wl.tokens).cuda()
+    stream = torch.cuda.current_stream()
+    nsb = enc.encode_all(wl.n_texts, tok, wl.cu_seqlens, wl.part_offsets, b_min, n_max, ptrs,
+                         policy=policy, stream=stream)
+    enc.check(stream)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), nsb
+
+
+def _oracle_rows(spec, weights, wl, idx):
+    w = E.as_f64(weights)
+    sh = spec.encoder
+    return E.encode_texts(w, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, idx, sh.ln_eps)
+
+
+def _sample(spec, wl, n_random, n_sb, seed=0):
+    """Texts to compare: SuperBatch ends, split-partition boundaries, random."""
+    sbs = OP.plan(wl.part_offsets, spec.b_min, spec.n_max, OP.R2)
+    idx = {0, wl.n_texts - 1}
+    for sb in sbs[:n_sb] + sbs[-2:]:
+        idx.update({sb.text_begin, sb.text_end - 1})
+    for sb in sbs:
+        for s in sb.segments:
+            if s.row_offset > 0:
+                idx.update({s.first_text - 1, s.first_text})
+    rng = np.random.default_rng(seed)
+    idx.update(rng.choice(wl.n_texts, size=n_random, replace=False).tolist())
+    return sorted(idx), sbs
+
+
+def test_tiny_all_texts():
+    torch = torch_cuda()
+    spec, wl, weights = _setup("tiny")
+    sh = spec.encoder
+    print(f"[tiny] texts={wl.n_texts} tokens={wl.n_tokens}", flush=True)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    got, nsb = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    assert nsb == 1
+    assert not np.isnan(got).any()
+    ref = _oracle_rows(spec, weights, wl, range(wl.n_texts))
+    assert_parity(got, ref, "tiny")
+    enc.close()
+
+
+def test_tiny_invariant_to_composition_and_chunking():
+    """A text's embedding is bit-identical whatever SuperBatch it lands in,
+    whatever policy formed the SuperBatches and wherever chunks are cut."""
+    torch = torch_cuda()
+    spec, wl, weights = _setup("tiny")
+    sh = spec.encoder
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    a, _ = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, 0)
+    b, nb = _encode_all(torch, enc, wl, sh.d_model, 37, 60)  # many SuperBatches, splits
+    c, nc = _encode_all(torch, enc, wl, sh.d_model, 100, 0, S.SURGE_POLICY_LITERAL)
+    enc.close()
+    small = S.Encoder(desc_of(sh), weight_list(sh, weights), 64)  # one text per chunk or so
+    d, _ = _encode_all(torch, small, wl, sh.d_model, spec.b_min, 0)
+    small.close()
+    assert nb > 10 and nc > 5
+    assert np.array_equal(a, b)
+    assert np.array_equal(a, c)
+    assert np.array_equal(a, d)
+
+
+def test_superbatch_entry_point_with_split_partition():
+    """surge_encode_superbatch with a hand-made segment table: a SuperBatch
+    holding the tail of one partition (row_offset > 0) and the head of the
+    next, written into partitions with guard rows left untouched."""
+    torch = torch_cuda()
+    spec, wl, weights = _setup("tiny")
+    sh = spec.encoder
+    d = sh.d_model
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    texts = list(range(100, 130))  # global texts 100..129
+    cu = wl.cu_seqlens[100:131] - wl.cu_seqlens[100]
+    tok = torch.from_numpy(wl.tokens[wl.cu_seqlens[100]:wl.cu_seqlens[130]].copy()).cuda()
+    part_sizes = np.array([50, 40], dtype=np.int64)
+    outs = [torch.full((n, d), float("nan"), device="cuda") for n in part_sizes]
+    ptrs = np.array([o.data_ptr() for o in outs], dtype=np.uint64)
+    segs = S.segments_array([(0, 12, 0, 38), (12, 18, 1, 0)])
+    enc.encode_superbatch(30, int(cu[-1]), tok, cu, segs, ptrs, part_sizes,
+                          stream=torch.cuda.current_stream())
+    enc.check()
+    torch.cuda.synchronize()
+    p0 = outs[0].cpu().numpy()
+    p1 = outs[1].cpu().numpy()
+    assert np.isnan(p0[:38]).all() and np.isnan(p1[18:]).all()
+    ref = _oracle_rows(spec, weights, wl, texts)
+    got = np.concatenate([p0[38:50], p1[:18]])
+    assert_parity(got, ref, "tiny")
+    enc.close()
+
+
+def test_edge_cases_empty_partitions_and_extreme_lengths():
+    torch = torch_cuda()
+    spec = W.WORKLOADS["tiny"]
+    sh = spec.encoder
+    lengths = [1, 64, 2, 64, 1, 3, 64, 1, 2, 33]
+    sizes = [0, 3, 0, 0, 5, 2, 0]
+    wl = W.workload_from_lengths(spec, sizes, lengths, seed=4)
+    weights = W.make_weights(sh, seed=1)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 128)
+    got, nsb = _encode_all(torch, enc, wl, sh.d_model, 2, 3)
+    assert not np.isnan(got).any()
+    ref = _oracle_rows(spec, weights, wl, range(wl.n_texts))
+    assert_parity(got, ref, "tiny")
+    # n_texts = 0 is a no-op.
+    empty = W.workload_from_lengths(spec, [0, 0], [], seed=4)
+    out = torch.zeros((1, sh.d_model), device="cuda")
+    enc.encode_all(0, out, empty.cu_seqlens, empty.part_offsets, 2, 3,
+                   np.array([out.data_ptr(), out.data_ptr()], dtype=np.uint64))
+    enc.close()
+
+
+def test_invalid_arguments_write_nothing():
+    torch = torch_cuda()
+    spec, wl, weights = _setup("tiny")
+    sh = spec.encoder
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    out, ptrs = _outputs(torch, wl, sh.d_model)
+    tok = torch.from_numpy(wl.tokens).cuda()
+    bad_cu = wl.cu_seqlens.copy()
+    bad_cu[5] = bad_cu[4]  # a zero-length text
+    with pytest.raises(S.SurgeError) as ei:
+        enc.encode_all(wl.n_texts, tok, bad_cu, wl.part_offsets, 1000, 0, ptrs)
+    assert ei.value.status == S.SURGE_ERR_INVALID_ARGUMENT
+    bad_ptrs = ptrs.copy()
+    bad_ptrs[3] += 4  # misaligned output
+    with pytest.raises(S.SurgeError):
+        enc.encode_all(wl.n_texts, tok, wl.cu_seqlens, wl.part_offsets, 1000, 0, bad_ptrs)
+    torch.cuda.synchronize()
+    assert torch.isnan(out).all()
+    enc.close()
+
+
+def test_out_of_vocab_token_is_reported():
+    torch = torch_cuda()
+    spec, wl, weights = _setup("tiny")
+    sh = spec.encoder
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    toks = wl.tokens.copy()
+    toks[10] = sh.vocab_size + 5
+    out, ptrs = _outputs(torch, wl, sh.d_model)
+    enc.encode_all(wl.n_texts, torch.from_numpy(toks).cuda(), wl.cu_seqlens, wl.part_offsets,
+                   1000, 0, ptrs)
+    with pytest.raises(S.SurgeError) as ei:
+        enc.check()
+    assert ei.value.status == S.SURGE_ERR_INVALID_ARGUMENT
+    enc.check()  # the flag is cleared
+    enc.close()
+
+
+@pytest.mark.parametrize("name,n_random,n_sb", [("minilm", 40, 8), ("bge", 24, 6),
+                                                ("minilm_heavy", 24, 8), ("large", 4, 2),
+                                                ("bge_s1", 8, 2)])
+def test_full_workload_sampled(name, n_random, n_sb):
+    torch = torch_cuda()
+    spec, wl, weights = _setup(name)
+    sh = spec.encoder
+    print(f"[{name}] texts={wl.n_texts} tokens={wl.n_tokens}", flush=True)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 18)
+    got, nsb = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    enc.close()
+    idx, sbs = _sample(spec, wl, n_random, n_sb)
+    assert nsb == len(sbs)
+    assert not np.isnan(got).any()
+    norms = np.linalg.norm(got.astype(np.float64), axis=1)
+    assert np.max(np.abs(norms - 1.0)) < 1e-5
+    ref = _oracle_rows(spec, weights, wl, idx)
+    assert_parity(got[idx], ref, name)
