@@ -11,9 +11,13 @@
 // Staging.  Each thread loads its share of stage k+1 (16-byte chunks) into
 // registers while stage k runs on the MFMA units, then writes it to the
 // other LDS buffer; one barrier per stage.  LDS rows are 128 B (64 bf16 of
-// K); the 16-byte chunk c of row r is stored at position c ^ (r & 7), so the
-// fragment reads (8 consecutive rows, same chunk) and the row writes hit
-// distinct banks.
+// K); the 16-byte chunk c of row r is stored at position
+// c ^ (r & 7) ^ ((r >> 3) & 1).  A fragment read takes the same chunk from
+// consecutive rows: any 8 aligned rows then land on 8 different 16-byte
+// positions and any 16 aligned rows on 16 different (row parity, position)
+// pairs, so the reads are free of bank conflicts whether the LDS serves a
+// 16-byte read 8 lanes at a time over 32 banks or 16 lanes at a time over
+// 64 banks.  Row writes (8 lanes per row, all chunks) are contiguous.
 //
 // Operand roles.  The MFMA A operand is the weight tile and B the token
 // tile, so the accumulators hold Y^T: each lane owns one token row and four
@@ -36,6 +40,10 @@ namespace {
 
 constexpr int BK = 64;
 
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
+}
+
 // Native 16-byte vector (HIP's uint4 is a union-based struct, which keeps
 // LLVM from turning the staging arrays into registers).
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -54,9 +62,14 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   constexpr int XI = BM * 8 / NT;  // 16-byte chunks per thread per stage, X tile
   constexpr int WI = BN * 8 / NT;  // ... W tile
   static_assert(XI * NT == BM * 8 && WI * NT == BN * 8, "tile/thread mismatch");
+  static_assert(NT % 128 == 0, "a thread's rows must share their phase mod 16");
 
-  __shared__ u32x4 sX[2][BM * 8];
-  __shared__ u32x4 sW[2][BN * 8];
+  // Main loop: stage b holds X rows at smem[b*SSTAGE ..] and W rows after
+  // them.  Epilogue: the same memory holds fp32 output rows.
+  constexpr int SSTAGE = (BM + BN) * 8;
+  __shared__ u32x4 smem[2 * SSTAGE];
+#define SX(b) (smem + (b) * SSTAGE)
+#define SW(b) (smem + (b) * SSTAGE + BM * 8)
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -76,13 +89,13 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   const int wm0 = (wave / WAVES_N) * WM;
 
   // Thread t copies chunks t, t + NT, ... of each tile: chunk c is row c/8,
-  // logical 16-byte column c%8, stored at column (c%8) ^ (row & 7).  NT is a
-  // multiple of 64, so every chunk of a thread has the same column and the
-  // same row phase, and its rows are NT/8 apart.
+  // logical 16-byte column c%8.  NT is a multiple of 128, so every chunk of
+  // a thread has the same column and the same row phase (row & 15), and its
+  // rows are NT/8 apart: its LDS slots are s_idx0 + j * NT.
   constexpr int RSTEP = NT / 8;
   const int row0 = threadIdx.x >> 3;
   const int kc = threadIdx.x & 7;
-  const int s_idx0 = row0 * 8 + (kc ^ (row0 & 7));
+  const int s_idx0 = swz(row0, kc);
   const u32x4* gw0 = reinterpret_cast<const u32x4*>(W + (size_t)(n0 + row0) * K) + kc;
   const size_t wstep = (size_t)RSTEP * K / 8;  // 16-byte units between a thread's W rows
   size_t xoff[XI];
@@ -111,86 +124,168 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
 #pragma unroll
   for (int j = 0; j < WI; ++j) rw[j] = gw0[j * wstep];
 #pragma unroll
-  for (int j = 0; j < XI; ++j) sX[0][s_idx0 + j * NT] = rx[j];
+  for (int j = 0; j < XI; ++j) SX(0)[s_idx0 + j * NT] = rx[j];
 #pragma unroll
-  for (int j = 0; j < WI; ++j) sW[0][s_idx0 + j * NT] = rw[j];
+  for (int j = 0; j < WI; ++j) SW(0)[s_idx0 + j * NT] = rw[j];
   __syncthreads();
 
+  // One 64-wide K stage per trip.  The body is branch-free (the last trip
+  // re-loads its own stage into the idle buffer) so that the instruction
+  // order below, pinned with scheduling group barriers, holds:
+  //   global loads of stage k+1 | LDS reads of step 0 |
+  //   steps 0..2: each MFMA followed by one LDS read of the next step |
+  //   step 3 MFMAs | LDS writes of stage k+1.
+  constexpr int NR = TN + TM;   // fragment reads per 16-wide step
+  constexpr int NM = TN * TM;   // MFMAs per step
+  static_assert(NM >= NR, "interleave needs at least one MFMA per read");
   for (int kt = 0; kt < nkt; ++kt) {
     const int buf = kt & 1;
-    const bool more = kt + 1 < nkt;
-    if (more) {
-      const int k8 = (kt + 1) * (BK / 8);
+    const int k8 = min(kt + 1, nkt - 1) * (BK / 8);
 #pragma unroll
-      for (int j = 0; j < XI; ++j) rx[j] = X4[xoff[j] + k8];
+    for (int j = 0; j < XI; ++j) rx[j] = X4[xoff[j] + k8];
 #pragma unroll
-      for (int j = 0; j < WI; ++j) rw[j] = gw0[j * wstep + k8];
-    }
+    for (int j = 0; j < WI; ++j) rw[j] = gw0[j * wstep + k8];
+
+    bf16x8 fa[2][TN], fb[2][TM];
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+      fa[0][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, lhi)]);
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      fb[0][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, lhi)]);
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
-      const int ch = ks * 2 + lhi;
-      bf16x8 a[TN], b[TM];
+      const int cur = ks & 1;
+      if (ks + 1 < BK / 16) {
+        const int ch = (ks + 1) * 2 + lhi;
 #pragma unroll
-      for (int i = 0; i < TN; ++i) {
-        const int row = wn0 + i * 32 + l32;
-        a[i] = __builtin_bit_cast(bf16x8, sW[buf][row * 8 + (ch ^ (row & 7))]);
-      }
+        for (int i = 0; i < TN; ++i)
+          fa[cur ^ 1][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, ch)]);
 #pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        const int row = wm0 + j * 32 + l32;
-        b[j] = __builtin_bit_cast(bf16x8, sX[buf][row * 8 + (ch ^ (row & 7))]);
+        for (int j = 0; j < TM; ++j)
+          fb[cur ^ 1][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, ch)]);
       }
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          acc[i][j] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
     }
-    if (more) {
 #pragma unroll
-      for (int j = 0; j < XI; ++j) sX[buf ^ 1][s_idx0 + j * NT] = rx[j];
+    for (int j = 0; j < XI; ++j) SX(buf ^ 1)[s_idx0 + j * NT] = rx[j];
 #pragma unroll
-      for (int j = 0; j < WI; ++j) sW[buf ^ 1][s_idx0 + j * NT] = rw[j];
+    for (int j = 0; j < WI; ++j) SW(buf ^ 1)[s_idx0 + j * NT] = rw[j];
+
+    // Pin the order described above.
+    __builtin_amdgcn_sched_group_barrier(0x020, XI + WI, 0);  // global loads
+    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);       // LDS reads, step 0
+#pragma unroll
+    for (int ks = 0; ks + 1 < BK / 16; ++ks) {
+#pragma unroll
+      for (int t = 0; t < NR; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
     }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);       // last step
+    __builtin_amdgcn_sched_group_barrier(0x200, XI + WI, 0);  // LDS writes
     __syncthreads();
   }
 
-  // Epilogue.  acc[i][j] register r holds Y[m][n] with
+  // Epilogue, staged through LDS so global traffic is whole rows.
+  // acc[i][j] register r holds Y[m][n] with
   //   m = m0 + wm0 + j*32 + lane%32
-  //   n = n0 + wn0 + i*32 + 8*(r/4) + 4*(lane/32) + r%4.
+  //   n = n0 + wn0 + i*32 + 8*(r/4) + 4*(lane/32) + r%4,
+  // i.e. registers 4g..4g+3 are the 8-byte output unit
+  // (wn0 + i*32 + 8g)/4 + lane/32 of row m (a row holds BN/4 such units).
+  // The LDS holds the BM x BN tile as bf16 rows of BN/4 8-byte units; unit
+  // u of row r sits at u ^ (r & 31), so the 32 rows an accumulator register
+  // spans fall on distinct banks and a 16-byte pair {2k, 2k+1} stays
+  // together (possibly with its halves swapped).
+  //   1. (residual only) every thread copies whole rows of R into the tile
+  //      with 16-byte coalesced loads, all issued before any is used;
+  //   2. each lane adds bias (+ GELU) to its accumulators, adds the residual
+  //      read back from the tile, rounds once to bf16 and writes the tile;
+  //   3. every thread stores whole rows of the tile with 16-byte stores.
+#undef SX
+#undef SW
+  {
+    static_assert(2 * (BM + BN) * 8 * 16 >= BM * BN * 2, "bf16 tile must fit the LDS");
+    constexpr int U = BN / 4;            // 8-byte units per row
+    constexpr int PAIRS = BN / 8;        // 16-byte pairs per row
+    constexpr int RPI = NT / PAIRS;      // rows per coalesced iteration
+    constexpr int ITER = BM / RPI;
+    static_assert(BM % RPI == 0 && U >= 32, "epilogue shape");
+    uint2* t8 = reinterpret_cast<uint2*>(smem);
+    u32x4* t16 = smem;
+    const int cp = threadIdx.x % PAIRS;  // this thread's 16-byte pair in a row
+    const int cr = threadIdx.x / PAIRS;
+    if (EPI == EPI_BIAS_RESIDUAL) {
+      u32x4 rv[ITER];
 #pragma unroll
-  for (int j = 0; j < TM; ++j) {
-    const int m = m0 + wm0 + j * 32 + l32;
-    if (m >= M) continue;
+      for (int it = 0; it < ITER; ++it) {
+        const int m = min(m0 + it * RPI + cr, M - 1);
+        rv[it] = *reinterpret_cast<const u32x4*>(R + (size_t)m * N + n0 + 8 * cp);
+      }
+#pragma unroll
+      for (int it = 0; it < ITER; ++it) {
+        const int r = it * RPI + cr;
+        const int ph = (2 * cp) ^ (r & 31);  // physical unit of logical unit 2cp
+        u32x4 v = rv[it];
+        if (ph & 1) v = u32x4{v[2], v[3], v[0], v[1]};
+        t16[r * PAIRS + (ph >> 1)] = v;
+      }
+      __syncthreads();
+    }
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = n0 + wn0 + i * 32 + g * 8 + lhi * 4;
-        const float4 bb = *reinterpret_cast<const float4*>(bias + n);
-        float v0 = acc[i][j][g * 4 + 0] + bb.x;
-        float v1 = acc[i][j][g * 4 + 1] + bb.y;
-        float v2 = acc[i][j][g * 4 + 2] + bb.z;
-        float v3 = acc[i][j][g * 4 + 3] + bb.w;
-        if (EPI == EPI_BIAS_GELU) {
-          v0 = gelu_erf(v0);
-          v1 = gelu_erf(v1);
-          v2 = gelu_erf(v2);
-          v3 = gelu_erf(v3);
+        const int u = (wn0 + i * 32 + 8 * g) / 4 + lhi;
+        const float4 bb = *reinterpret_cast<const float4*>(bias + n0 + 4 * u);
+#pragma unroll
+        for (int j = 0; j < TM; ++j) {
+          const int r = wm0 + j * 32 + l32;
+          float o0 = acc[i][j][4 * g + 0] + bb.x;
+          float o1 = acc[i][j][4 * g + 1] + bb.y;
+          float o2 = acc[i][j][4 * g + 2] + bb.z;
+          float o3 = acc[i][j][4 * g + 3] + bb.w;
+          if (EPI == EPI_BIAS_GELU) {
+            o0 = gelu_erf(o0);
+            o1 = gelu_erf(o1);
+            o2 = gelu_erf(o2);
+            o3 = gelu_erf(o3);
+          }
+          uint2& cell = t8[r * U + (u ^ (r & 31))];
+          if (EPI == EPI_BIAS_RESIDUAL) {
+            const uint2 rr = cell;
+            o0 += __uint_as_float(rr.x << 16);
+            o1 += __uint_as_float(rr.x & 0xffff0000u);
+            o2 += __uint_as_float(rr.y << 16);
+            o3 += __uint_as_float(rr.y & 0xffff0000u);
+          }
+          uint2 out;
+          out.x = pack_bf16x2(o0, o1);
+          out.y = pack_bf16x2(o2, o3);
+          cell = out;
         }
-        const size_t o = (size_t)m * N + n;
-        if (EPI == EPI_BIAS_RESIDUAL) {
-          const uint2 rr = *reinterpret_cast<const uint2*>(R + o);
-          v0 += __uint_as_float(rr.x << 16);
-          v1 += __uint_as_float(rr.x & 0xffff0000u);
-          v2 += __uint_as_float(rr.y << 16);
-          v3 += __uint_as_float(rr.y & 0xffff0000u);
-        }
-        uint2 out;
-        out.x = pack_bf16x2(v0, v1);
-        out.y = pack_bf16x2(v2, v3);
-        *reinterpret_cast<uint2*>(Y + o) = out;
       }
+    }
+    __syncthreads();
+    u32x4 ov[ITER];
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int r = it * RPI + cr;
+      const int ph = (2 * cp) ^ (r & 31);
+      ov[it] = t16[r * PAIRS + (ph >> 1)];
+      if (ph & 1) ov[it] = u32x4{ov[it][2], ov[it][3], ov[it][0], ov[it][1]};
+    }
+#pragma unroll
+    for (int it = 0; it < ITER; ++it) {
+      const int m = m0 + it * RPI + cr;
+      if (m < M) *reinterpret_cast<u32x4*>(Y + (size_t)m * N + n0 + 8 * cp) = ov[it];
     }
   }
 }
@@ -225,11 +320,11 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
 hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                          uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  // 256 x 256 tiles (8 waves of 128 tokens x 64 features) where the feature
+  // 256 x 256 tiles (8 waves of 64 tokens x 128 features) where the feature
   // count allows it and there are enough token rows to fill the chip;
   // 128 x 128 tiles (4 waves of 64 x 64) otherwise.
   if (N % 256 == 0 && M >= 8192)
-    return launch_tiles<256, 256, 2, 4>(X, W, bias, R, Y, M, N, K, epi, stream);
+    return launch_tiles<256, 256, 4, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
   return launch_tiles<128, 128, 2, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
 }
 
