@@ -49,7 +49,8 @@ surge_status surge_op_linear(int64_t M, int32_t N, int32_t K, const uint16_t* d_
  * out[rows of text i, head h] = softmax(Q_h K_h^T / sqrt(d_head)) V_h.
  * d_qkv bf16 [T, 3 n_heads d_head] (Q | K | V blocks, head h at columns
  * h d_head of each); d_out bf16 [T, n_heads d_head]; T = cu[n_texts].
- * d_head is 32 or 64; n_heads * d_head % 128 == 0.
+ * d_head is 32 or 64; n_heads * d_head % 128 == 0; every text length in
+ * [1, 4096].
  */
 surge_status surge_op_attention(int64_t n_texts, const int64_t* h_cu_seqlens, int32_t n_heads,
                                 int32_t d_head, const uint16_t* d_qkv, uint16_t* d_out,

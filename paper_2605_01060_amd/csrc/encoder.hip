@@ -57,6 +57,7 @@ struct surge_encoder {
   uint16_t *X = nullptr, *QKV = nullptr, *CTX = nullptr, *Y = nullptr, *H = nullptr;
   int32_t* d_cu = nullptr;     // [max_tokens + 1]
   uint64_t* d_dst = nullptr;   // [max_tokens]
+  uint32_t* d_items = nullptr; // [max_tokens] attention work items
   int* d_err = nullptr;
   // pinned staging ring for chunk metadata
   void* staging[kStagingSlots] = {};
@@ -66,6 +67,7 @@ struct surge_encoder {
   size_t staging_bytes = 0;
   // host scratch
   std::vector<uint64_t> h_dst;
+  std::vector<int64_t> h_lcu;
   // profiling
   bool prof = false;
   std::vector<hipEvent_t> prof_events;
@@ -149,17 +151,26 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
     const int64_t S = t1 - t0;
     const int64_t T = cu[t1] - cu[t0];
 
-    // Stage (cu32 [S+1], dst [S]) in a pinned slot, then copy to the device.
+    // Stage (cu32 [S+1], dst [S], attention items) in a pinned slot, then
+    // copy to the device.
     const int slot = e->staging_next;
     e->staging_next = (slot + 1) % kStagingSlots;
     if (e->staging_used[slot]) HIP_TRY(hipEventSynchronize(e->staging_ev[slot]));
-    const size_t cu_bytes = align_up((size_t)(S + 1) * 4, 16);
-    int32_t* hcu = (int32_t*)e->staging[slot];
-    uint64_t* hdst = (uint64_t*)((char*)e->staging[slot] + align_up((size_t)(e->max_tokens + 1) * 4, 16));
+    char* stg = (char*)e->staging[slot];
+    const size_t cu_region = align_up((size_t)(e->max_tokens + 1) * 4, 16);
+    const size_t dst_region = (size_t)e->max_tokens * 8;
+    int32_t* hcu = (int32_t*)stg;
+    uint64_t* hdst = (uint64_t*)(stg + cu_region);
+    uint32_t* hitems = (uint32_t*)(stg + cu_region + dst_region);
     for (int64_t i = 0; i <= S; ++i) hcu[i] = (int32_t)(cu[t0 + i] - cu[t0]);
     memcpy(hdst, e->h_dst.data() + t0, (size_t)S * 8);
+    e->h_lcu.resize((size_t)S + 1);
+    for (int64_t i = 0; i <= S; ++i) e->h_lcu[(size_t)i] = cu[t0 + i] - cu[t0];
+    const int n_items = attention_items(e->h_lcu.data(), S, hitems);
+    const size_t cu_bytes = align_up((size_t)(S + 1) * 4, 16);
     HIP_TRY(hipMemcpyAsync(e->d_cu, hcu, cu_bytes, hipMemcpyHostToDevice, stream));
     HIP_TRY(hipMemcpyAsync(e->d_dst, hdst, (size_t)S * 8, hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipMemcpyAsync(e->d_items, hitems, (size_t)n_items * 4, hipMemcpyHostToDevice, stream));
     HIP_TRY(hipEventRecord(e->staging_ev[slot], stream));
     e->staging_used[slot] = true;
 
@@ -180,7 +191,7 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
       LAUNCH(SURGE_KERNEL_QKV, 2.0 * Td * d * 3 * d, 2.0 * (Td * d + 3.0 * d * d + Td * 3 * d),
              launch_linear(e->X, w.wqkv, w.bqkv, nullptr, e->QKV, T, 3 * d, d, EPI_BIAS, stream));
       LAUNCH(SURGE_KERNEL_ATTN, 4.0 * d * sumL2, 2.0 * Td * 4 * d,
-             launch_attention(e->QKV, e->CTX, e->d_cu, Si, D.n_heads, dh, stream));
+             launch_attention(e->QKV, e->CTX, e->d_cu, e->d_items, n_items, D.n_heads, dh, stream));
       LAUNCH(SURGE_KERNEL_OPROJ, 2.0 * Td * d * d, 2.0 * (3.0 * Td * d + (double)d * d),
              launch_linear(e->CTX, w.wo, w.bo, e->X, e->Y, T, d, d, EPI_BIAS_RESIDUAL, stream));
       LAUNCH(SURGE_KERNEL_LN1, 0.0, 4.0 * Td * d,
@@ -239,9 +250,9 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
                 (long long)expect, n_weights);
   for (int i = 0; i < n_weights; ++i)
     if (!host_weights[i]) return fail(SURGE_ERR_INVALID_ARGUMENT, "weight %d is NULL", i);
-  if (max_tokens_per_chunk < D.max_positions || max_tokens_per_chunk > (int64_t)1 << 30)
+  if (max_tokens_per_chunk < D.max_positions || max_tokens_per_chunk > (int64_t)1 << 25)
     return fail(SURGE_ERR_INVALID_ARGUMENT,
-                "max_tokens_per_chunk=%lld outside [max_positions, 2^30]",
+                "max_tokens_per_chunk=%lld outside [max_positions, 2^25]",
                 (long long)max_tokens_per_chunk);
 
   surge_encoder* e = new surge_encoder();
@@ -367,6 +378,7 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   wtake((size_t)T * f * 2);        // H
   wtake((size_t)(T + 1) * 4 + 16); // cu
   wtake((size_t)T * 8);            // dst
+  wtake((size_t)T * 4);            // attention items
   wtake(256);                      // err
   err = hipMalloc(&e->wsblock, ws);
   if (err != hipSuccess)
@@ -381,12 +393,13 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   e->H = (uint16_t*)(w + wo[4]);
   e->d_cu = (int32_t*)(w + wo[5]);
   e->d_dst = (uint64_t*)(w + wo[6]);
-  e->d_err = (int*)(w + wo[7]);
+  e->d_items = (uint32_t*)(w + wo[7]);
+  e->d_err = (int*)(w + wo[8]);
   err = hipMemset(e->d_err, 0, 256);
   if (err != hipSuccess)
     return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipMemset failed: %s", hipGetErrorString(err)));
 
-  e->staging_bytes = align_up((size_t)(T + 1) * 4, 16) + (size_t)T * 8;
+  e->staging_bytes = align_up((size_t)(T + 1) * 4, 16) + (size_t)T * 8 + (size_t)T * 4;
   for (int i = 0; i < kStagingSlots; ++i) {
     err = hipHostMalloc(&e->staging[i], e->staging_bytes, hipHostMallocDefault);
     if (err != hipSuccess)

@@ -25,9 +25,15 @@ hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias
 
 // Packed varlen multi-head self-attention.  qkv bf16 [T, 3 H dh] (Q | K | V
 // column blocks, head h at columns h*dh of each), out bf16 [T, H dh].
-// Attention runs within each text only.  dh is 32 or 64.
-hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* cu, int n_texts,
-                            int n_heads, int d_head, hipStream_t stream);
+// Attention runs within each text only.  dh is 32 or 64.  items lists the
+// (text << 7 | 32-query block) work items built by attention_items.
+hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* cu,
+                            const uint32_t* items, int n_items, int n_heads, int d_head,
+                            hipStream_t stream);
+
+// Work items of a chunk (at most cu[n_texts] of them, every text length in
+// [1, 4096]), longest text first.  Returns the item count.
+int attention_items(const int64_t* cu, int64_t n_texts, uint32_t* items);
 
 // y = LN(x) per row of d (d % 8 == 0, d <= 1024), bf16 in/out.
 hipError_t launch_layernorm(const uint16_t* x, const float* gamma, const float* beta, float eps,

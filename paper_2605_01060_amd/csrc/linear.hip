@@ -44,10 +44,6 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
 }
 
-// Native 16-byte vector (HIP's uint4 is a union-based struct, which keeps
-// LLVM from turning the staging arrays into registers).
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, const float* __restrict__ bias,

@@ -114,10 +114,16 @@ surge_status surge_op_attention(int64_t n_texts, const int64_t* cu, int32_t n_he
     return fail(SURGE_ERR_INVALID_ARGUMENT, "device buffers must be 16-byte aligned");
   DeviceCu dcu;
   int64_t T = 0;
-  surge_status st = upload_cu(n_texts, cu, 1 << 16, &dcu, &T);
+  surge_status st = upload_cu(n_texts, cu, 4096, &dcu, &T);
   if (st != SURGE_OK) return st;
+  std::vector<uint32_t> items((size_t)T);
+  const int n_items = attention_items(cu, n_texts, items.data());
+  DeviceCu ditems;
+  HIP_TRY(hipMalloc(&ditems.ptr, (size_t)n_items * 4));
+  HIP_TRY(hipMemcpy(ditems.ptr, items.data(), (size_t)n_items * 4, hipMemcpyHostToDevice));
   hipStream_t s = (hipStream_t)hip_stream;
-  HIP_TRY(launch_attention(d_qkv, d_out, dcu.ptr, (int)n_texts, n_heads, d_head, s));
+  HIP_TRY(launch_attention(d_qkv, d_out, dcu.ptr, (const uint32_t*)ditems.ptr, n_items, n_heads,
+                           d_head, s));
   HIP_TRY(hipStreamSynchronize(s));
   return SURGE_OK;
 }
