@@ -44,7 +44,29 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI>
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds):
+// the wave's 64 lanes land contiguously at LDS byte address `lds` (wave
+// uniform, passed in M0).  Issued as inline assembly so that the waits are
+// placed by the kernel itself (s_waitcnt vmcnt before the barrier that
+// publishes a stage); the compiler cannot prove which stage an in-flight
+// copy targets and would otherwise wait for it before every LDS read.
+__device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(g), "s"(lds)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool DTL>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, const float* __restrict__ bias,
     const uint16_t* __restrict__ R, uint16_t* __restrict__ Y, int M, int N, int K, int tiles_n,
@@ -114,6 +136,85 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   const int l32 = lane & 31;
   const int lhi = lane >> 5;
 
+  if constexpr (DTL) {
+    // Lane l of wave w, copy j, fills LDS slot p = (j*NWAVES + w)*64 + l of
+    // a tile: row p/8, stored chunk l%8.  Its logical chunk is
+    // (l%8) ^ (row&7) ^ ((row>>3)&1) = (l%8) ^ (l/8) ^ (w&1), the same for
+    // every j (NWAVES is even); its rows are NWAVES*8 apart.
+    constexpr int DSTEP = NWAVES * 8;
+    const int drow = wave * 8 + (lane >> 3);
+    const int dch = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
+    const uint16_t* xg[XI];
+#pragma unroll
+    for (int j = 0; j < XI; ++j)
+      xg[j] = X + (size_t)min(m0 + drow + j * DSTEP, M - 1) * K + dch * 8;
+    const uint16_t* wg = W + (size_t)(n0 + drow) * K + dch * 8;
+    const size_t wgstep = (size_t)DSTEP * K;
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem) + wave * 64 * 16);
+    constexpr uint32_t STAGE_BYTES = SSTAGE * 16;
+    constexpr uint32_t COPY_BYTES = NWAVES * 64 * 16;
+
+#define SURGE_ISSUE_STAGE(kk_, b_)                                                              \
+    do {                                                                                        \
+      const int ko_ = (kk_) * BK;                                                               \
+      const uint32_t base_ = lds0 + (uint32_t)(b_) * STAGE_BYTES;                               \
+      _Pragma("unroll") for (int j = 0; j < XI; ++j)                                            \
+        copy_to_lds16(xg[j] + ko_, base_ + j * COPY_BYTES);                                     \
+      _Pragma("unroll") for (int j = 0; j < WI; ++j)                                            \
+        copy_to_lds16(wg + j * wgstep + ko_, base_ + BM * 8 * 16 + j * COPY_BYTES);             \
+    } while (0)
+
+    SURGE_ISSUE_STAGE(0, 0);
+    wait_copies();
+    __syncthreads();
+    constexpr int NR = TN + TM;
+    constexpr int NM = TN * TM;
+    static_assert(NM >= NR, "interleave needs at least one MFMA per read");
+    for (int kt = 0; kt < nkt; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < nkt) SURGE_ISSUE_STAGE(kt + 1, buf ^ 1);
+      bf16x8 fa[2][TN], fb[2][TM];
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+        fa[0][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, lhi)]);
+#pragma unroll
+      for (int j = 0; j < TM; ++j)
+        fb[0][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, lhi)]);
+#pragma unroll
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        const int cur = ks & 1;
+        if (ks + 1 < BK / 16) {
+          const int ch = (ks + 1) * 2 + lhi;
+#pragma unroll
+          for (int i = 0; i < TN; ++i)
+            fa[cur ^ 1][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, ch)]);
+#pragma unroll
+          for (int j = 0; j < TM; ++j)
+            fb[cur ^ 1][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, ch)]);
+        }
+#pragma unroll
+        for (int i = 0; i < TN; ++i)
+#pragma unroll
+          for (int j = 0; j < TM; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
+                                                                0, 0, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
+#pragma unroll
+      for (int ks = 0; ks + 1 < BK / 16; ++ks) {
+#pragma unroll
+        for (int t = 0; t < NR; ++t) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
+      wait_copies();
+      __syncthreads();
+    }
+#undef SURGE_ISSUE_STAGE
+  } else {
   u32x4 rx[XI], rw[WI];
 #pragma unroll
   for (int j = 0; j < XI; ++j) rx[j] = X4[xoff[j]];
@@ -188,6 +289,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
     __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);       // last step
     __builtin_amdgcn_sched_group_barrier(0x200, XI + WI, 0);  // LDS writes
     __syncthreads();
+  }
+
   }
 
   // Epilogue, staged through LDS so global traffic is whole rows.
@@ -286,7 +389,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N>
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool DTL = false>
 hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                         uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream) {
   const int tiles_n = N / BN;
@@ -296,15 +399,15 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
   const dim3 block(WAVES_M * WAVES_N * 64);
   switch (epi) {
     case EPI_BIAS:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS>), grid, block, 0,
+      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS, DTL>), grid, block, 0,
                          stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
     case EPI_BIAS_GELU:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_GELU>), grid,
+      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_GELU, DTL>), grid,
                          block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
     default:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL>), grid,
+      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL, DTL>), grid,
                          block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
   }
@@ -320,8 +423,8 @@ hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias
   // count allows it and there are enough token rows to fill the chip;
   // 128 x 128 tiles (4 waves of 64 x 64) otherwise.
   if (N % 256 == 0 && M >= 8192)
-    return launch_tiles<256, 256, 4, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
-  return launch_tiles<128, 128, 2, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
+    return launch_tiles<256, 256, 4, 2, true>(X, W, bias, R, Y, M, N, K, epi, stream);
+  return launch_tiles<128, 128, 2, 2, true>(X, W, bias, R, Y, M, N, K, epi, stream);
 }
 
 }  // namespace surge
