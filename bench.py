@@ -21,6 +21,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
+from paper_2605_01060_amd import profiling  # noqa: E402
 from paper_2605_01060_amd import surge as S  # noqa: E402
 from paper_2605_01060_amd import workload as W  # noqa: E402
 
@@ -84,10 +85,13 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="bge", choices=sorted(W.WORKLOADS))
-    ap.add_argument("--chunk-tokens", type=int, default=1 << 18)
+    ap.add_argument("--chunk-tokens", type=int, default=1 << 20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-events", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=0,
+                    help="run one plain device-to-device copy of this many MiB before the "
+                         "warm-up (reference for FETCH_SIZE / WRITE_SIZE counter runs)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -113,6 +117,14 @@ def main(argv=None):
                     dtype=np.uint64)
     stream = torch.cuda.current_stream()
     flops = encoder_flops(sh, wl.lengths)
+    if args.copy_calibration_mb > 0:
+        n = args.copy_calibration_mb << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         return enc.encode_all(wl.n_texts, tok, wl.cu_seqlens, wl.part_offsets, spec.b_min,
@@ -155,21 +167,27 @@ def main(argv=None):
             ent["gbs"] = s["bytes"] / (s["total_ms"] / 1e3) / 1e9
         kernels[name] = ent
     roofline = None
+    traffic_class = {"qkv": "qkv", "ffn1": "ffn1", "oproj": "residual", "ffn2": "residual",
+                     "attn": "attn", "ln1": "layernorm", "ln2": "layernorm"}
     if kernels:
         dom = max(kernels, key=lambda k: kernels[k]["total_ms_per_step"])
         s = kstats[dom]
+        traffic = None
+        if dom in traffic_class:
+            traffic = profiling.load_traffic(traffic_class[dom], args.workload)
         if dom in MFMA_KERNELS:
             achieved = s["flops"] / (s["total_ms"] / 1e3) / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
                         "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                        "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                         "per_launch_flops": s["flops"] / s["launches"],
+                        "per_launch_algorithmic_bytes": s["bytes"] / s["launches"],
                         "avg_launch_ms": s["total_ms"] / s["launches"]}
         else:
             achieved = s["bytes"] / (s["total_ms"] / 1e3) / 1e9
             roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                        "traffic": None, "per_launch_bytes": s["bytes"] / s["launches"],
+                        "traffic": traffic, "per_launch_bytes": s["bytes"] / s["launches"],
                         "avg_launch_ms": s["total_ms"] / s["launches"]}
 
     cpu = None

@@ -62,11 +62,48 @@ __device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
 
 __device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Tile order.  Workgroups are dispatched round-robin over the 8 XCDs
+// (block b runs on XCD b % 8), each with its own 4 MB L2, so the order in
+// which one XCD walks its tiles decides what its L2 can reuse.
+//   ORDER_ROW_GROUPS: each XCD walks a contiguous eighth of the tile grid in
+//     groups of 8 token-row blocks, feature tile outer: a weight tile is
+//     reused by 8 row blocks and 8 X row blocks stay resident meanwhile.
+//   ORDER_FEATURE_HALVES: the XCDs form 2 feature halves x 4 token-row
+//     quarters and each walks its rectangle as above, so an XCD touches half
+//     of W (FFN1's 4.7 MB W does not fit one L2, half of it does).  Falls
+//     back to ORDER_ROW_GROUPS when the rectangles do not divide evenly.
+// The blocks beyond the last full eighth keep their own index.
+constexpr int ORDER_ROW_GROUPS = 0;
+constexpr int ORDER_FEATURE_HALVES = 1;
+
+template <int ORDER>
+__device__ __forceinline__ void tile_coords(int b, int n_tiles, int tiles_n, int* tm, int* tn) {
+  const int tiles_m = n_tiles / tiles_n;
+  const int xcd = b & 7;
+  const int local = b >> 3;
+  int t, m_base = 0, n_base = 0, m_cnt = tiles_m, n_cnt = tiles_n;
+  if (ORDER == ORDER_FEATURE_HALVES && tiles_n % 2 == 0 && tiles_m % 4 == 0) {
+    n_cnt = tiles_n / 2;
+    m_cnt = tiles_m / 4;
+    n_base = (xcd & 1) * n_cnt;
+    m_base = (xcd >> 1) * m_cnt;
+    t = local;
+  } else {
+    const int per_xcd = n_tiles >> 3;
+    t = b < (per_xcd << 3) ? xcd * per_xcd + local : b;
+  }
+  const int grp = t / (8 * n_cnt);
+  const int in = t - grp * 8 * n_cnt;
+  const int rows = min(8, m_cnt - grp * 8);
+  *tn = n_base + in / rows;
+  *tm = m_base + grp * 8 + in % rows;
+}
+
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool DTL>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool DTL, int ORDER>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, const float* __restrict__ bias,
     const uint16_t* __restrict__ R, uint16_t* __restrict__ Y, int M, int N, int K, int tiles_n,
@@ -92,15 +129,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
 
-  // XCD-aware tile order (see header).
-  int tile = blockIdx.x;
-  {
-    const int per_xcd = n_tiles >> 3;
-    const int full = per_xcd << 3;
-    if (tile < full) tile = (tile & 7) * per_xcd + (tile >> 3);
-  }
-  const int tn = tile % tiles_n;
-  const int tm = tile / tiles_n;
+  int tn, tm;
+  tile_coords<ORDER>(blockIdx.x, n_tiles, tiles_n, &tm, &tn);
   const int m0 = tm * BM;
   const int n0 = tn * BN;
   const int wn0 = (wave % WAVES_N) * WN;
@@ -389,7 +419,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool DTL = false>
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool DTL>
 hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                         uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream) {
   const int tiles_n = N / BN;
@@ -399,16 +429,18 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
   const dim3 block(WAVES_M * WAVES_N * 64);
   switch (epi) {
     case EPI_BIAS:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS, DTL>), grid, block, 0,
-                         stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
+      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS, DTL, ORDER_ROW_GROUPS>),
+                         grid, block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
     case EPI_BIAS_GELU:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_GELU, DTL>), grid,
-                         block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
+      hipLaunchKernelGGL(
+          (linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_GELU, DTL, ORDER_FEATURE_HALVES>), grid,
+          block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
     default:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL, DTL>), grid,
-                         block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
+      hipLaunchKernelGGL(
+          (linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL, DTL, ORDER_ROW_GROUPS>), grid,
+          block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
   }
   return hipGetLastError();

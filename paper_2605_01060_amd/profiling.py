@@ -1,0 +1,142 @@
+"""Turn rocprofv3 output into the short summaries kept under profiles/.
+
+    python -m paper_2605_01060_amd.profiling stats KERNEL_STATS_CSV --command "..."
+    python -m paper_2605_01060_amd.profiling traffic FETCH_CSV WRITE_CSV \
+        --kernel-class ffn1 --copy-mib 2048 --command-fetch "..." --command-write "..."
+
+`stats` renders a kernel-trace `*_kernel_stats.csv` as a markdown table.
+`traffic` reads two `--pmc` runs (FETCH_SIZE, then WRITE_SIZE, KiB per
+dispatch), scales each by what the same counter reads for the plain device
+copy of known size that the benchmark runs first (`--copy-calibration-mb`),
+and reports HBM bytes per launch of one kernel class, together with the
+SHA-256 of the kernel's source file so that a stale figure is recognisable.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+from typing import Dict, List, Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+
+# kernel class -> (source file, predicate on the demangled kernel name)
+KERNEL_CLASSES = {
+    "qkv": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) == 0),
+    "ffn1": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) == 1),
+    "residual": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) == 2),
+    "attn": ("attention.hip", lambda n: "attention_varlen_kernel" in n),
+    "layernorm": ("rows.hip", lambda n: "layernorm_kernel" in n),
+}
+COPY_KERNEL = "copyBuffer"
+
+
+def _epi(name: str) -> int:
+    m = re.search(r"linear_bf16_kernel<\d+, \d+, \d+, \d+, (\d+)", name)
+    return int(m.group(1)) if m else -1
+
+
+def source_hash(kernel_class: str) -> str:
+    fname = KERNEL_CLASSES[kernel_class][0]
+    h = hashlib.sha256()
+    for f in (fname, "device_common.h"):
+        with open(os.path.join(PKG, "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def stats_markdown(path: str, command: str, top: int = 12) -> str:
+    rows = list(csv.DictReader(open(path)))
+    out = [f"Command: `{command}`", "", "| kernel | calls | mean µs | total ms | % |",
+           "|---|---|---|---|---|"]
+    for r in rows[:top]:
+        name = r["Name"]
+        short = name.replace("surge::(anonymous namespace)::", "").replace("void ", "")
+        short = re.sub(r"\(.*", "", short)
+        out.append(f"| `{short}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                   f"{float(r['TotalDurationNs']) / 1e6:.1f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
+
+
+def _per_dispatch(path: str, counter: str) -> Dict[str, List[float]]:
+    vals: Dict[str, List[float]] = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return vals
+
+
+def traffic(fetch_csv: str, write_csv: str, kernel_class: str, copy_mib: float) -> Dict:
+    pred = KERNEL_CLASSES[kernel_class][1]
+    res = {"kernel_class": kernel_class, "copy_bytes": copy_mib * 2 ** 20,
+           "source_sha256": source_hash(kernel_class)}
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"),
+                               ("write", write_csv, "WRITE_SIZE")):
+        vals = _per_dispatch(path, counter)
+        copy = [v for n, vs in vals.items() if COPY_KERNEL in n for v in vs]
+        if not copy:
+            raise SystemExit(f"no {COPY_KERNEL} dispatch in {path}")
+        copy_kib = max(copy)  # the calibration copy is the largest copy dispatch
+        scale = (copy_mib * 1024.0) / copy_kib
+        ks = [v for n, vs in vals.items() if pred(n) for v in vs]
+        if not ks:
+            raise SystemExit(f"no {kernel_class} dispatch in {path}")
+        res[f"{key}_kib_per_dispatch_raw"] = statistics.fmean(ks)
+        res[f"{key}_copy_kib"] = copy_kib
+        res[f"{key}_scale"] = scale
+        res[f"{key}_bytes_per_launch"] = statistics.fmean(ks) * 1024.0 * scale
+        res[f"{key}_dispatches"] = len(ks)
+    res["bytes_per_launch"] = res["fetch_bytes_per_launch"] + res["write_bytes_per_launch"]
+    return res
+
+
+def load_traffic(kernel_class: str, workload: str) -> Optional[float]:
+    """HBM bytes per launch recorded under profiles/, or None if absent or if
+    the kernel's source changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha256") != source_hash(kernel_class):
+        return None
+    return float(rec["bytes_per_launch"])
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    a = sub.add_parser("stats")
+    a.add_argument("csv")
+    a.add_argument("--command", required=True)
+    b = sub.add_parser("traffic")
+    b.add_argument("fetch_csv")
+    b.add_argument("write_csv")
+    b.add_argument("--kernel-class", required=True, choices=sorted(KERNEL_CLASSES))
+    b.add_argument("--copy-mib", type=float, required=True)
+    b.add_argument("--command-fetch", required=True)
+    b.add_argument("--command-write", required=True)
+    args = ap.parse_args(argv)
+    if args.cmd == "stats":
+        sys.stdout.write(stats_markdown(args.csv, args.command))
+    else:
+        rec = traffic(args.fetch_csv, args.write_csv, args.kernel_class, args.copy_mib)
+        sys.stdout.write(
+            f"HBM traffic of the `{args.kernel_class}` kernel class (mean per launch), from\n\n"
+            f"- `{args.command_fetch}`\n- `{args.command_write}`\n\n"
+            "Each counter is scaled by what it reads for the benchmark's calibration copy "
+            f"({args.copy_mib:.0f} MiB device-to-device, the `{COPY_KERNEL}` dispatch).\n\n"
+            f"```json\n{json.dumps(rec, indent=1)}\n```\n")
+
+
+if __name__ == "__main__":
+    main()

@@ -272,7 +272,7 @@ class Encoder:
     """Owns a surge_encoder; weights are the fp32 arrays of the fixed order."""
 
     def __init__(self, desc: EncoderDesc, weights: Sequence[np.ndarray],
-                 max_tokens_per_chunk: int = 1 << 18):
+                 max_tokens_per_chunk: int = 1 << 20):
         self.desc = desc
         self.handle = surge_encoder_create(desc, weights, max_tokens_per_chunk)
 

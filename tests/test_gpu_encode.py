@@ -200,7 +200,7 @@ def test_full_workload_sampled(name, n_random, n_sb):
     spec, wl, weights = _setup(name)
     sh = spec.encoder
     print(f"[{name}] texts={wl.n_texts} tokens={wl.n_tokens}", flush=True)
-    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 18)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 20)  # the benchmark's chunk
     got, nsb = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, spec.n_max)
     enc.close()
     idx, sbs = _sample(spec, wl, n_random, n_sb)
