@@ -66,27 +66,27 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// erf(x) by Abramowitz & Stegun, Handbook of Mathematical Functions,
-// formula 7.1.26: for x >= 0, erf(x) = 1 - (a1 t + ... + a5 t^5) exp(-x^2)
-// with t = 1 / (1 + p x); absolute error <= 1.5e-7 (about 6e-7 evaluated
-// in fp32 with the hardware reciprocal and exp2), far below the bf16
-// rounding of the outputs it feeds.  Odd symmetry for x < 0.
-__device__ __forceinline__ float erf_as7126(float x) {
-  const float ax = fabsf(x);
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, ax, 1.0f));
-  float poly = fmaf(1.061405429f, t, -1.453152027f);
-  poly = fmaf(poly, t, 1.421413741f);
-  poly = fmaf(poly, t, -0.284496736f);
-  poly = fmaf(poly, t, 0.254829592f);
-  poly *= t;
-  const float e = __builtin_amdgcn_exp2f(-ax * ax * 1.4426950408889634f);
-  const float y = fmaf(-poly, e, 1.0f);
-  return copysignf(y, x);
-}
-
-// GELU, z * Phi(z) = 0.5 z (1 + erf(z / sqrt 2)).
+// GELU, z Phi(z) = 0.5 z (1 + erf(z / sqrt 2)), with erf by Abramowitz &
+// Stegun, Handbook of Mathematical Functions, formula 7.1.26: for x >= 0,
+// erf(x) = 1 - t (a1 + a2 t + ... + a5 t^4) exp(-x^2), t = 1 / (1 + p x),
+// absolute error <= 1.5e-7 (about 6e-7 evaluated in fp32 with the hardware
+// reciprocal and exp2), far below the bf16 rounding of the outputs it
+// feeds.  With q = 0.5 |z| t (a1 + ... + a5 t^4) exp(-z^2 / 2), both signs
+// of z give GELU(z) = max(z, 0) - q (for z < 0, 1 + erf = 1 - (1 - 2q/|z|)),
+// so the 0.5 and 1/sqrt 2 fold into the constants and no sign fix-up is
+// needed.
 __device__ __forceinline__ float gelu_erf(float z) {
-  return 0.5f * z * (1.0f + erf_as7126(z * 0.70710678118654752f));
+  constexpr float P = 0.3275911f * 0.70710678118654752f;
+  constexpr float A1 = 0.5f * 0.254829592f, A2 = 0.5f * -0.284496736f, A3 = 0.5f * 1.421413741f,
+                  A4 = 0.5f * -1.453152027f, A5 = 0.5f * 1.061405429f;
+  const float az = fabsf(z);
+  const float t = __builtin_amdgcn_rcpf(fmaf(P, az, 1.0f));
+  float poly = fmaf(A5, t, A4);
+  poly = fmaf(poly, t, A3);
+  poly = fmaf(poly, t, A2);
+  poly = fmaf(poly, t, A1);
+  const float e = __builtin_amdgcn_exp2f(z * z * -0.72134752044448170f);  // exp(-z^2 / 2)
+  return fmaf(-(az * poly) * t, e, fmaxf(z, 0.0f));
 }
 
 }  // namespace surge

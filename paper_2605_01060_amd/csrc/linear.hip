@@ -6,42 +6,47 @@
 // Tiling.  A workgroup computes a BM x BN tile of Y (tokens x features) with
 // WAVES_M x WAVES_N waves; each wave owns a (BM/WAVES_M) x (BN/WAVES_N)
 // sub-tile held as 32 x 32 v_mfma_f32_32x32x16_bf16 accumulators.  K is
-// walked in 64-wide stages through a double-buffered LDS tile.
+// walked in BK-wide stages (64 or 32) through a double-buffered LDS tile.
 //
-// Staging.  Each thread loads its share of stage k+1 (16-byte chunks) into
-// registers while stage k runs on the MFMA units, then writes it to the
-// other LDS buffer; one barrier per stage.  LDS rows are 128 B (64 bf16 of
-// K); the 16-byte chunk c of row r is stored at position
-// c ^ (r & 7) ^ ((r >> 3) & 1).  A fragment read takes the same chunk from
-// consecutive rows: any 8 aligned rows then land on 8 different 16-byte
-// positions and any 16 aligned rows on 16 different (row parity, position)
-// pairs, so the reads are free of bank conflicts whether the LDS serves a
-// 16-byte read 8 lanes at a time over 32 banks or 16 lanes at a time over
-// 64 banks.  Row writes (8 lanes per row, all chunks) are contiguous.
+// Staging.  Stage k+1 is copied straight from global memory into the idle
+// LDS buffer (global_load_lds_dwordx4, 1 KB per wave instruction) while
+// stage k runs on the MFMA units; one wait and one barrier per stage.  An
+// LDS row holds BK bf16 of one X or W row as CPR = BK/8 16-byte chunks; the
+// logical chunk c of row r is stored at position c ^ f(r), with
+//   CPR = 8: f(r) = (r & 7) ^ ((r >> 3) & 1),
+//   CPR = 4: f(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1).
+// A fragment read takes one logical chunk from 32 consecutive rows; with
+// either f, any 8 aligned rows fall on 8 different 16-byte slots of a
+// 128-byte window and any 16 aligned rows on 16 different slots of a
+// 256-byte window, so the reads are free of bank conflicts whether the LDS
+// serves a 16-byte read 8 lanes at a time over 32 banks or 16 lanes at a
+// time over 64 banks.  A copy instruction writes 64 consecutive slots, so
+// each lane fetches the logical chunk that belongs in its slot.
+//
+// Occupancy.  Every configuration runs 2 waves per SIMD.  8-wave 256 x 256
+// tiles take the whole CU (128 KB of LDS); 4-wave tiles with BK = 32 need
+// at most 64 KB, so two workgroups share a CU and one's epilogue overlaps
+// the other's MFMA loop.
 //
 // Operand roles.  The MFMA A operand is the weight tile and B the token
 // tile, so the accumulators hold Y^T: each lane owns one token row and four
 // consecutive features per register group, which makes the epilogue (bias,
 // GELU, residual, bf16 store) 8-byte vector accesses.
 //
-// Order.  Workgroups are dispatched round-robin over the 8 XCDs; the tile
-// index is remapped so each XCD walks a contiguous range of token-row
-// blocks, all feature tiles of a row block back to back, keeping that row
-// block in the XCD's L2 while its feature tiles run.
-//
 // Every output row is computed from its own input row with a fixed K order
 // (no split-K, no atomics), so a text's result does not depend on which
-// other texts share its SuperBatch or chunk.
+// other texts share its SuperBatch or chunk, nor on the tile configuration.
 #include "device_common.h"
 #include "kernels.h"
 
 namespace surge {
 namespace {
 
-constexpr int BK = 64;
-
+template <int CPR>
 __device__ __forceinline__ int swz(int row, int chunk) {
-  return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
+  static_assert(CPR == 8 || CPR == 4, "LDS rows of 64 or 32 bf16");
+  if (CPR == 8) return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
+  return row * 4 + (chunk ^ ((row >> 1) & 3) ^ ((row >> 3) & 1));
 }
 
 // Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds):
@@ -60,7 +65,18 @@ __device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
       : "memory", "m0");
 }
 
-__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Wait until at most `later` stages' copies (CPS instructions each) issued
+// after the one needed next are still in flight.  The vector memory counter
+// retires a wave's loads in issue order.
+template <int CPS>
+__device__ __forceinline__ void wait_copies(int later) {
+  if (later <= 0)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if (later == 1)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(CPS) : "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * CPS) : "memory");
+}
 
 // Tile order.  Workgroups are dispatched round-robin over the 8 XCDs
 // (block b runs on XCD b % 8), each with its own 4 MB L2, so the order in
@@ -103,28 +119,32 @@ __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, bool DTL, int ORDER>
-__global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
-    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, const float* __restrict__ bias,
-    const uint16_t* __restrict__ R, uint16_t* __restrict__ Y, int M, int N, int K, int tiles_n,
-    int n_tiles) {
+template <int BM, int BN, int BK, int NBUF, int WAVES_M, int WAVES_N, int EPI, int ORDER>
+__global__ __launch_bounds__(WAVES_M* WAVES_N * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+                        const float* __restrict__ bias, const uint16_t* __restrict__ R,
+                        uint16_t* __restrict__ Y, int M, int N, int K, int tiles_n, int n_tiles) {
   constexpr int NWAVES = WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M;  // tokens per wave
   constexpr int WN = BN / WAVES_N;  // features per wave
   constexpr int TM = WM / 32;       // 32-token accumulator tiles per wave
   constexpr int TN = WN / 32;       // 32-feature accumulator tiles per wave
   constexpr int NT = NWAVES * 64;
-  constexpr int XI = BM * 8 / NT;  // 16-byte chunks per thread per stage, X tile
-  constexpr int WI = BN * 8 / NT;  // ... W tile
-  static_assert(XI * NT == BM * 8 && WI * NT == BN * 8, "tile/thread mismatch");
-  static_assert(NT % 128 == 0, "a thread's rows must share their phase mod 16");
+  constexpr int CPR = BK / 8;       // 16-byte chunks per LDS row
+  constexpr int RPC = 64 / CPR;     // rows one wave copy instruction fills
+  constexpr int XI = BM / (RPC * NWAVES);  // copy instructions per wave per stage, X tile
+  constexpr int WI = BN / (RPC * NWAVES);  // ... W tile
+  static_assert(XI * RPC * NWAVES == BM && WI * RPC * NWAVES == BN, "tile/wave mismatch");
+  static_assert(CPR == 4 || NWAVES % 2 == 0, "copy slot phase needs an even wave count");
+  static_assert(NBUF >= 2 && NBUF <= 4, "2 to 4 LDS stage buffers");
+  static_assert((XI + WI) * (NBUF - 2) < 64, "copies in flight must fit the counter");
 
-  // Main loop: stage b holds X rows at smem[b*SSTAGE ..] and W rows after
-  // them.  Epilogue: the same memory holds fp32 output rows.
-  constexpr int SSTAGE = (BM + BN) * 8;
-  __shared__ u32x4 smem[2 * SSTAGE];
-#define SX(b) (smem + (b) * SSTAGE)
-#define SW(b) (smem + (b) * SSTAGE + BM * 8)
+  // Main loop: NBUF stage buffers; buffer b holds X rows at
+  // smem[b*SSTAGE ..] and W rows after them.  Epilogue: the same memory
+  // holds the bf16 output tile.
+  constexpr int SSTAGE = (BM + BN) * CPR;
+  constexpr int SMEM = NBUF * SSTAGE > BM * BN / 8 ? NBUF * SSTAGE : BM * BN / 8;
+  __shared__ u32x4 smem[SMEM];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -135,24 +155,6 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   const int n0 = tn * BN;
   const int wn0 = (wave % WAVES_N) * WN;
   const int wm0 = (wave / WAVES_N) * WM;
-
-  // Thread t copies chunks t, t + NT, ... of each tile: chunk c is row c/8,
-  // logical 16-byte column c%8.  NT is a multiple of 128, so every chunk of
-  // a thread has the same column and the same row phase (row & 15), and its
-  // rows are NT/8 apart: its LDS slots are s_idx0 + j * NT.
-  constexpr int RSTEP = NT / 8;
-  const int row0 = threadIdx.x >> 3;
-  const int kc = threadIdx.x & 7;
-  const int s_idx0 = swz(row0, kc);
-  const u32x4* gw0 = reinterpret_cast<const u32x4*>(W + (size_t)(n0 + row0) * K) + kc;
-  const size_t wstep = (size_t)RSTEP * K / 8;  // 16-byte units between a thread's W rows
-  size_t xoff[XI];
-#pragma unroll
-  for (int j = 0; j < XI; ++j) {
-    const int xrow = min(m0 + row0 + j * RSTEP, M - 1);  // rows past M read clamped, never stored
-    xoff[j] = (size_t)xrow * (K / 8) + kc;
-  }
-  const u32x4* X4 = reinterpret_cast<const u32x4*>(X);
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -166,149 +168,88 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   const int l32 = lane & 31;
   const int lhi = lane >> 5;
 
-  if constexpr (DTL) {
-    // Lane l of wave w, copy j, fills LDS slot p = (j*NWAVES + w)*64 + l of
-    // a tile: row p/8, stored chunk l%8.  Its logical chunk is
-    // (l%8) ^ (row&7) ^ ((row>>3)&1) = (l%8) ^ (l/8) ^ (w&1), the same for
-    // every j (NWAVES is even); its rows are NWAVES*8 apart.
-    constexpr int DSTEP = NWAVES * 8;
-    const int drow = wave * 8 + (lane >> 3);
-    const int dch = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
-    const uint16_t* xg[XI];
+  // Lane l of wave w, copy j, fills LDS slot p = (j*NWAVES + w)*64 + l of a
+  // tile: row p / CPR, stored chunk l % CPR.  Its logical chunk
+  // (l % CPR) ^ f(row) is the same for every j:
+  //   CPR = 8: (l & 7) ^ (l >> 3) ^ (w & 1)   (NWAVES even),
+  //   CPR = 4: (l & 3) ^ ((l >> 3) & 3) ^ (l >> 5).
+  // Its rows are NWAVES * RPC apart.
+  constexpr int DSTEP = NWAVES * RPC;
+  const int drow = wave * RPC + lane / CPR;
+  const int dch = CPR == 8 ? (lane & 7) ^ (lane >> 3) ^ (wave & 1)
+                           : (lane & 3) ^ ((lane >> 3) & 3) ^ (lane >> 5);
+  const uint16_t* xg[XI];
 #pragma unroll
-    for (int j = 0; j < XI; ++j)
-      xg[j] = X + (size_t)min(m0 + drow + j * DSTEP, M - 1) * K + dch * 8;
-    const uint16_t* wg = W + (size_t)(n0 + drow) * K + dch * 8;
-    const size_t wgstep = (size_t)DSTEP * K;
-    const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem) + wave * 64 * 16);
-    constexpr uint32_t STAGE_BYTES = SSTAGE * 16;
-    constexpr uint32_t COPY_BYTES = NWAVES * 64 * 16;
+  for (int j = 0; j < XI; ++j)
+    xg[j] = X + (size_t)min(m0 + drow + j * DSTEP, M - 1) * K + dch * 8;  // rows past M: clamped, never stored
+  const uint16_t* wg = W + (size_t)(n0 + drow) * K + dch * 8;
+  const size_t wgstep = (size_t)DSTEP * K;
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_address(smem) + wave * 64 * 16);
+  constexpr uint32_t STAGE_BYTES = SSTAGE * 16;
+  constexpr uint32_t COPY_BYTES = NWAVES * 64 * 16;
 
-#define SURGE_ISSUE_STAGE(kk_, b_)                                                              \
-    do {                                                                                        \
-      const int ko_ = (kk_) * BK;                                                               \
-      const uint32_t base_ = lds0 + (uint32_t)(b_) * STAGE_BYTES;                               \
-      _Pragma("unroll") for (int j = 0; j < XI; ++j)                                            \
-        copy_to_lds16(xg[j] + ko_, base_ + j * COPY_BYTES);                                     \
-      _Pragma("unroll") for (int j = 0; j < WI; ++j)                                            \
-        copy_to_lds16(wg + j * wgstep + ko_, base_ + BM * 8 * 16 + j * COPY_BYTES);             \
-    } while (0)
+#define SURGE_ISSUE_STAGE(kk_, b_)                                                        \
+  do {                                                                                    \
+    const int ko_ = (kk_) * BK;                                                           \
+    const uint32_t base_ = lds0 + (uint32_t)(b_) * STAGE_BYTES;                           \
+    _Pragma("unroll") for (int j = 0; j < XI; ++j)                                        \
+      copy_to_lds16(xg[j] + ko_, base_ + j * COPY_BYTES);                                 \
+    _Pragma("unroll") for (int j = 0; j < WI; ++j)                                        \
+      copy_to_lds16(wg + j * wgstep + ko_, base_ + BM * CPR * 16 + j * COPY_BYTES);       \
+  } while (0)
 
-    SURGE_ISSUE_STAGE(0, 0);
-    wait_copies();
-    __syncthreads();
-    constexpr int NR = TN + TM;
-    constexpr int NM = TN * TM;
-    static_assert(NM >= NR, "interleave needs at least one MFMA per read");
-    for (int kt = 0; kt < nkt; ++kt) {
-      const int buf = kt & 1;
-      if (kt + 1 < nkt) SURGE_ISSUE_STAGE(kt + 1, buf ^ 1);
-      bf16x8 fa[2][TN], fb[2][TM];
+  // Prologue: stages 0 .. NBUF-1 in flight; wait for stage 0, publish it
+  // and read its first fragments.
+#pragma unroll
+  for (int st = 0; st < NBUF; ++st)
+    if (st < nkt) SURGE_ISSUE_STAGE(st, st);
+  wait_copies<XI + WI>(min(NBUF - 1, nkt - 1));
+  __syncthreads();
+  constexpr int S = BK / 16;   // 16-wide MFMA steps per stage
+  constexpr int NR = TN + TM;  // fragment reads per step
+  constexpr int NM = TN * TM;  // MFMAs per step
+  static_assert(S % 2 == 0, "fragment parity must restart at every stage");
+  static_assert(NM >= NR, "interleave needs at least one MFMA per read");
+  bf16x8 fa[2][TN], fb[2][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+    fa[0][i] = __builtin_bit_cast(bf16x8, smem[BM * CPR + swz<CPR>(wn0 + i * 32 + l32, lhi)]);
+#pragma unroll
+  for (int j = 0; j < TM; ++j)
+    fb[0][j] = __builtin_bit_cast(bf16x8, smem[swz<CPR>(wm0 + j * 32 + l32, lhi)]);
+
+  // One stage per trip.  Steps 0 .. S-2 run their MFMAs with the fragment
+  // reads of the following step interleaved one by one (pinned with
+  // scheduling group barriers).  Then the wave waits for its copies of
+  // stage k+1 and all waves meet: stage k+1 is published and nobody reads
+  // stage k's buffer any more, so the copies of stage k+NBUF go into it.
+  // The last step's MFMAs, which need no LDS, run after the barrier while
+  // the first fragments of stage k+1 are read, so the MFMA pipe does not
+  // wait for LDS at the stage boundary.  (On the last trip those reads hit
+  // a stale buffer and are discarded.)
+  int cur_buf = 0;
+  for (int kt = 0; kt < nkt; ++kt) {
+    const u32x4* sx = smem + cur_buf * SSTAGE;
+    const u32x4* sw = sx + BM * CPR;
+#pragma unroll
+    for (int ks = 0; ks + 1 < S; ++ks) {
+      const int cur = ks & 1;
+      const int ch = (ks + 1) * 2 + lhi;
 #pragma unroll
       for (int i = 0; i < TN; ++i)
-        fa[0][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, lhi)]);
+        fa[cur ^ 1][i] = __builtin_bit_cast(bf16x8, sw[swz<CPR>(wn0 + i * 32 + l32, ch)]);
 #pragma unroll
       for (int j = 0; j < TM; ++j)
-        fb[0][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, lhi)]);
-#pragma unroll
-      for (int ks = 0; ks < BK / 16; ++ks) {
-        const int cur = ks & 1;
-        if (ks + 1 < BK / 16) {
-          const int ch = (ks + 1) * 2 + lhi;
-#pragma unroll
-          for (int i = 0; i < TN; ++i)
-            fa[cur ^ 1][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, ch)]);
-#pragma unroll
-          for (int j = 0; j < TM; ++j)
-            fb[cur ^ 1][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, ch)]);
-        }
-#pragma unroll
-        for (int i = 0; i < TN; ++i)
-#pragma unroll
-          for (int j = 0; j < TM; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j],
-                                                                0, 0, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);
-#pragma unroll
-      for (int ks = 0; ks + 1 < BK / 16; ++ks) {
-#pragma unroll
-        for (int t = 0; t < NR; ++t) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);
-      wait_copies();
-      __syncthreads();
-    }
-#undef SURGE_ISSUE_STAGE
-  } else {
-  u32x4 rx[XI], rw[WI];
-#pragma unroll
-  for (int j = 0; j < XI; ++j) rx[j] = X4[xoff[j]];
-#pragma unroll
-  for (int j = 0; j < WI; ++j) rw[j] = gw0[j * wstep];
-#pragma unroll
-  for (int j = 0; j < XI; ++j) SX(0)[s_idx0 + j * NT] = rx[j];
-#pragma unroll
-  for (int j = 0; j < WI; ++j) SW(0)[s_idx0 + j * NT] = rw[j];
-  __syncthreads();
-
-  // One 64-wide K stage per trip.  The body is branch-free (the last trip
-  // re-loads its own stage into the idle buffer) so that the instruction
-  // order below, pinned with scheduling group barriers, holds:
-  //   global loads of stage k+1 | LDS reads of step 0 |
-  //   steps 0..2: each MFMA followed by one LDS read of the next step |
-  //   step 3 MFMAs | LDS writes of stage k+1.
-  constexpr int NR = TN + TM;   // fragment reads per 16-wide step
-  constexpr int NM = TN * TM;   // MFMAs per step
-  static_assert(NM >= NR, "interleave needs at least one MFMA per read");
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
-    const int k8 = min(kt + 1, nkt - 1) * (BK / 8);
-#pragma unroll
-    for (int j = 0; j < XI; ++j) rx[j] = X4[xoff[j] + k8];
-#pragma unroll
-    for (int j = 0; j < WI; ++j) rw[j] = gw0[j * wstep + k8];
-
-    bf16x8 fa[2][TN], fb[2][TM];
-#pragma unroll
-    for (int i = 0; i < TN; ++i)
-      fa[0][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, lhi)]);
-#pragma unroll
-    for (int j = 0; j < TM; ++j)
-      fb[0][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, lhi)]);
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      const int cur = ks & 1;
-      if (ks + 1 < BK / 16) {
-        const int ch = (ks + 1) * 2 + lhi;
-#pragma unroll
-        for (int i = 0; i < TN; ++i)
-          fa[cur ^ 1][i] = __builtin_bit_cast(bf16x8, SW(buf)[swz(wn0 + i * 32 + l32, ch)]);
-#pragma unroll
-        for (int j = 0; j < TM; ++j)
-          fb[cur ^ 1][j] = __builtin_bit_cast(bf16x8, SX(buf)[swz(wm0 + j * 32 + l32, ch)]);
-      }
+        fb[cur ^ 1][j] = __builtin_bit_cast(bf16x8, sx[swz<CPR>(wm0 + j * 32 + l32, ch)]);
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j)
-          acc[i][j] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cur][i], fb[cur][j], acc[i][j], 0,
+                                                              0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < XI; ++j) SX(buf ^ 1)[s_idx0 + j * NT] = rx[j];
-#pragma unroll
-    for (int j = 0; j < WI; ++j) SW(buf ^ 1)[s_idx0 + j * NT] = rw[j];
-
-    // Pin the order described above.
-    __builtin_amdgcn_sched_group_barrier(0x020, XI + WI, 0);  // global loads
-    __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);       // LDS reads, step 0
-#pragma unroll
-    for (int ks = 0; ks + 1 < BK / 16; ++ks) {
+    for (int ks = 0; ks + 1 < S; ++ks) {
 #pragma unroll
       for (int t = 0; t < NR; ++t) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
@@ -316,12 +257,33 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
       }
       __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, NM, 0);       // last step
-    __builtin_amdgcn_sched_group_barrier(0x200, XI + WI, 0);  // LDS writes
+    // stages issued after stage kt+1: up to kt + NBUF - 1, capped at the end
+    wait_copies<XI + WI>(min(kt + NBUF - 1, nkt - 1) - (kt + 1));
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this stage's reads are done
     __syncthreads();
+    if (kt + NBUF < nkt) SURGE_ISSUE_STAGE(kt + NBUF, cur_buf);
+    cur_buf = cur_buf + 1 == NBUF ? 0 : cur_buf + 1;
+    const u32x4* nx = smem + cur_buf * SSTAGE;
+    const u32x4* nw = nx + BM * CPR;
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+      fa[0][i] = __builtin_bit_cast(bf16x8, nw[swz<CPR>(wn0 + i * 32 + l32, lhi)]);
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      fb[0][j] = __builtin_bit_cast(bf16x8, nx[swz<CPR>(wm0 + j * 32 + l32, lhi)]);
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[1][i], fb[1][j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int t = 0; t < NR; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
   }
-
-  }
+#undef SURGE_ISSUE_STAGE
 
   // Epilogue, staged through LDS so global traffic is whole rows.
   // acc[i][j] register r holds Y[m][n] with
@@ -338,11 +300,8 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   //   2. each lane adds bias (+ GELU) to its accumulators, adds the residual
   //      read back from the tile, rounds once to bf16 and writes the tile;
   //   3. every thread stores whole rows of the tile with 16-byte stores.
-#undef SX
-#undef SW
   {
-    static_assert(2 * (BM + BN) * 8 * 16 >= BM * BN * 2, "bf16 tile must fit the LDS");
-    constexpr int U = BN / 4;            // 8-byte units per row
+        constexpr int U = BN / 4;            // 8-byte units per row
     constexpr int PAIRS = BN / 8;        // 16-byte pairs per row
     constexpr int RPI = NT / PAIRS;      // rows per coalesced iteration
     constexpr int ITER = BM / RPI;
@@ -419,7 +378,7 @@ __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) void linear_bf16_kernel(
   }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool DTL>
+template <int BM, int BN, int BK, int NBUF, int WAVES_M, int WAVES_N>
 hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                         uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream) {
   const int tiles_n = N / BN;
@@ -429,17 +388,17 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
   const dim3 block(WAVES_M * WAVES_N * 64);
   switch (epi) {
     case EPI_BIAS:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS, DTL, ORDER_ROW_GROUPS>),
+      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, EPI_BIAS, ORDER_ROW_GROUPS>),
                          grid, block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
     case EPI_BIAS_GELU:
       hipLaunchKernelGGL(
-          (linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_GELU, DTL, ORDER_FEATURE_HALVES>), grid,
+          (linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, EPI_BIAS_GELU, ORDER_FEATURE_HALVES>), grid,
           block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
     default:
       hipLaunchKernelGGL(
-          (linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL, DTL, ORDER_ROW_GROUPS>), grid,
+          (linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL, ORDER_ROW_GROUPS>), grid,
           block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
       break;
   }
@@ -455,8 +414,8 @@ hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias
   // count allows it and there are enough token rows to fill the chip;
   // 128 x 128 tiles (4 waves of 64 x 64) otherwise.
   if (N % 256 == 0 && M >= 8192)
-    return launch_tiles<256, 256, 4, 2, true>(X, W, bias, R, Y, M, N, K, epi, stream);
-  return launch_tiles<128, 128, 2, 2, true>(X, W, bias, R, Y, M, N, K, epi, stream);
+    return launch_tiles<256, 256, 64, 2, 4, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
+  return launch_tiles<128, 128, 64, 2, 2, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
 }
 
 }  // namespace surge

@@ -38,8 +38,10 @@ COPY_KERNEL = "copyBuffer"
 
 
 def _epi(name: str) -> int:
-    m = re.search(r"linear_bf16_kernel<\d+, \d+, \d+, \d+, (\d+)", name)
-    return int(m.group(1)) if m else -1
+    """Epilogue of a linear kernel instance: the template argument before
+    the tile order (the last one)."""
+    m = re.search(r"linear_bf16_kernel<([^>]*)>", name)
+    return int(m.group(1).split(",")[-2]) if m else -1
 
 
 def source_hash(kernel_class: str) -> str:
