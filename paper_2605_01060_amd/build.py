@@ -25,8 +25,11 @@ LIB = os.path.join(PKG, "libsurge.so")
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
           f"-I{INCLUDE}", f"-I{CSRC}"]
-# Packed fp32 VALU forms are kept out of the generated code.
-HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed fp32 VALU forms are kept out of the generated code.  MFMA
+# accumulators live in ordinary VGPRs, so code that scales them between
+# MFMAs (the attention softmax) needs no AGPR round trips.
+HIP_FLAGS = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+             "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def hipcc() -> str:

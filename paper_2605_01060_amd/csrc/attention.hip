@@ -7,19 +7,28 @@
 //
 // Work decomposition.  A work item is (text, 32-query block); the host
 // lists the items of a chunk longest text first, so the long texts start
-// early and the short ones fill in behind them.  One wave handles one item
-// for one head: it walks the text's keys in 32-key blocks with an online
-// softmax, prefetching the next block's K fragments and V rows into
-// registers while the current block is on the MFMA units.
+// early and the short ones fill in behind them.  One wave (a workgroup of
+// its own) handles one item for one head: it walks the text's keys in
+// 32-key blocks with an online softmax.
+//
+// Memory path.  A head's slice of a token row is DH contiguous bf16 (128 B
+// for DH = 64).  Q, K and V blocks move from global memory to LDS with
+// direct copies that read whole rows (8 lanes per 128-byte row), stored in
+// the conflict-free chunk swizzle; the next K/V block is copied into the
+// second LDS buffer while the current one is on the MFMA units.  The output
+// block is staged in LDS and written back as whole rows too.  (Reading the
+// MFMA operands straight from global memory would touch 32 rows per
+// instruction for 32 bytes each, which stalls the address path.)
 //
 // Scores are computed transposed, S^T = K Q^T, with
 // v_mfma_f32_32x32x16_bf16 so that every lane owns one query column: the
 // running max, the running sum and the rescaling of the output are per-lane
 // scalars, combined with the partner lane (lane ^ 32) that holds the other
 // half of the key block.  The probabilities stay in registers in exactly
-// the operand layout the P V product needs (O^T = V^T P^T); the V block is
-// staged through LDS so each lane can read the keys its MFMA slots stand
-// for.
+// the operand layout the P V product needs (O^T = V^T P^T); its V^T operand
+// is read from the row-major V block with the gfx950 transposing LDS read
+// (ds_read_b64_tr_b16), which hands each lane one feature of 4 consecutive
+// keys.
 #include <math.h>
 
 #include "device_common.h"
@@ -34,12 +43,18 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
                                                               const int32_t* __restrict__ cu,
                                                               const uint32_t* __restrict__ items,
                                                               int n_heads, float scale_log2) {
-  constexpr int KSTEPS = DH / 16;      // MFMA steps over the head dimension for S
-  constexpr int DT = DH / 32;          // 32-row tiles of O^T
-  constexpr int VCH = 32 * DH / 8;     // 16-byte chunks of a 32-key V block
-  constexpr int VPL = VCH / 64;        // ... per lane
-  constexpr int CPR = DH / 8;          // 16-byte chunks per V row
-  __shared__ uint16_t sV[32 * DH];
+  constexpr int KSTEPS = DH / 16;  // MFMA steps over the head dimension for S
+  constexpr int DT = DH / 32;      // 32-row tiles of O^T
+  constexpr int CPR = DH / 8;      // 16-byte chunks per row
+  constexpr int RPC = 64 / CPR;    // rows one wave copy fills
+  constexpr int NCP = 32 / RPC;    // copies per 32-row block
+  constexpr int BLK = 32 * CPR;    // 16-byte slots per 32-row block
+  // Two K/V buffers.  The Q block passes through the second K buffer before
+  // the first prefetch, and the output block is staged in the first one.
+  __shared__ u32x4 sK[2][BLK];
+  __shared__ u32x4 sV[2][BLK];
+  u32x4* const sQ = sK[1];
+  u32x4* const sO = sK[0];
 
   const int h = blockIdx.x % n_heads;
   const uint32_t item = items[blockIdx.x / n_heads];
@@ -51,35 +66,49 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
   const int beg = cu[t];
   const int L = cu[t + 1] - beg;
   const int D = n_heads * DH;
-  const size_t ld = (size_t)3 * D;
+  const int ld = 3 * D;
   const uint16_t* Qb = qkv + (size_t)beg * ld + (size_t)h * DH;
   const uint16_t* Kb = Qb + D;
   const uint16_t* Vb = Qb + 2 * D;
 
-  const int q = min(q0 + col, L - 1);
+  // Copy j of a 32-row block starting at row r0: lane l fills slot
+  // j*64 + l, i.e. row r0 + j*RPC + l/CPR with its swizzled chunk.  Rows past
+  // the text are read clamped (their scores are masked, their outputs not
+  // stored).
+  const int crow = lane / CPR;
+#define SURGE_COPY_BLOCK(src_, r0_, lds_)                                                   \
+  do {                                                                                      \
+    _Pragma("unroll") for (int j = 0; j < NCP; ++j) {                                       \
+      const int row_ = min((r0_) + j * RPC + crow, L - 1);                                  \
+      copy_to_lds16((src_) + __umul24(row_, ld) + copy_chunk<CPR>(lane, j) * 8,             \
+                    (lds_) + j * 1024);                                                     \
+    }                                                                                       \
+  } while (0)
+
+  const uint32_t lq = lds_address(sK[1]);
+  const uint32_t lk = lds_address(sK[0]);
+  const uint32_t lv = lds_address(sV[0]);
+  constexpr uint32_t BUF = BLK * 16;
+  SURGE_COPY_BLOCK(Qb, q0, lq);
+  SURGE_COPY_BLOCK(Kb, 0, lk);
+  SURGE_COPY_BLOCK(Vb, 0, lv);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
   bf16x8 qf[KSTEPS];
 #pragma unroll
   for (int kk = 0; kk < KSTEPS; ++kk)
-    qf[kk] = as_bf16x8(*reinterpret_cast<const uint4*>(Qb + (size_t)q * ld + kk * 16 + half * 8));
+    qf[kk] = __builtin_bit_cast(bf16x8, sQ[swz<CPR>(col, kk * 2 + half)]);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // Q is in registers: sK[1] is free
 
-  // Prefetch registers for one key block: K fragments (rows = keys) and the
-  // lane's share of the V rows (rows past the text are read clamped; their
-  // probabilities are zero).
-  u32x4 kf[KSTEPS], vr[VPL];
-#define SURGE_LOAD_KV_BLOCK(k0_)                                                              \
-  do {                                                                                        \
-    const int kr_ = min((k0_) + col, L - 1);                                                  \
-    _Pragma("unroll") for (int kk = 0; kk < KSTEPS; ++kk) kf[kk] =                            \
-        *reinterpret_cast<const u32x4*>(Kb + (size_t)kr_ * ld + kk * 16 + half * 8);          \
-    _Pragma("unroll") for (int c = 0; c < VPL; ++c) {                                         \
-      const int idx_ = lane + 64 * c;                                                         \
-      const int row_ = min((k0_) + idx_ / CPR, L - 1);                                        \
-      vr[c] = *(reinterpret_cast<const u32x4*>(Vb + (size_t)row_ * ld) + idx_ % CPR);         \
-    }                                                                                         \
-  } while (0)
-  SURGE_LOAD_KV_BLOCK(0);
+  // Transposing V reads: lane l supplies the address of 4 features of key
+  // 4*half + (l%16)/4 (+ 8 for the second read, + 16c) starting at feature
+  // dt*32 + 16*((l/16)%2) + 4*(l%4), and receives feature dt*32 + l%32 of
+  // the 4 keys 4*half + 4i..4i+3 of its 16-lane group, i.e. operand slots
+  // 4i..4i+3 of key 16c + 8i + 4*half + 0..3.
+  const int tr_key = 4 * half + ((lane & 15) >> 2);
+  const int tr_feat = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  float m_run = -INFINITY;
+  float m_run = -INFINITY;  // running max, log2 units (raw score x scale_log2)
   float l_run = 0.0f;
   f32x16 o[DT];
 #pragma unroll
@@ -87,15 +116,16 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[dt][r] = 0.0f;
 
+  int b = 0;
   for (int k0 = 0; k0 < L; k0 += 32) {
-    // Consume the prefetched block, then start loading the next one.
-    bf16x8 kc[KSTEPS];
-#pragma unroll
-    for (int kk = 0; kk < KSTEPS; ++kk) kc[kk] = __builtin_bit_cast(bf16x8, kf[kk]);
-    __syncthreads();  // the previous block's P V reads of sV are done
-#pragma unroll
-    for (int c = 0; c < VPL; ++c) reinterpret_cast<u32x4*>(sV)[lane + 64 * c] = vr[c];
-    if (k0 + 32 < L) SURGE_LOAD_KV_BLOCK(k0 + 32);
+    if (k0 > 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // block k0 is in LDS
+    if (k0 + 32 < L) {
+      // The other buffer's reads (previous block) were consumed by MFMAs.
+      SURGE_COPY_BLOCK(Kb, k0 + 32, lk + (b ^ 1) * BUF);
+      SURGE_COPY_BLOCK(Vb, k0 + 32, lv + (b ^ 1) * BUF);
+    }
+    const u32x4* kb = sK[b];
+    const u32x4* vb = sV[b];
 
     // S^T block: rows = keys k0..k0+31 (A operand = K), cols = queries.
     f32x16 s;
@@ -103,34 +133,39 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
     for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kc[kk], qf[kk], s, 0, 0, 0);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          __builtin_bit_cast(bf16x8, kb[swz<CPR>(col, kk * 2 + half)]), qf[kk], s, 0, 0, 0);
 
-    // Register r holds the score of key k0 + 8*(r/4) + 4*half + r%4.
-    float mloc = -INFINITY;
+    // Register r holds the score of key k0 + 8*(r/4) + 4*half + r%4; only
+    // the text's last block has keys past its end (uniform branch).
+    if (k0 + 32 > L) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = k0 + 8 * (r >> 2) + 4 * half + (r & 3);
-      s[r] = key < L ? s[r] * scale_log2 : -INFINITY;
-      mloc = fmaxf(mloc, s[r]);
+      for (int r = 0; r < 16; ++r)
+        if (k0 + 8 * (r >> 2) + 4 * half + (r & 3) >= L) s[r] = -INFINITY;
     }
+    float mloc = s[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    const float m_new = fmaxf(m_run, mloc * scale_log2);
     float psum = 0.0f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      s[r] = __builtin_amdgcn_exp2f(s[r] - m_new);
+      s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -m_new));
       psum += s[r];
     }
     psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
+    if (k0 == 0) {
+      l_run = psum;  // o is still zero: nothing to rescale
+    } else {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run = fmaf(l_run, alpha, psum);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+    }
     m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-
-    __syncthreads();  // sV written
 
     // O^T += V^T P^T over two 16-key halves c: slot j of this lane is key
     // 16c + 8*(j/4) + 4*half + j%4, the same key for the P (B) and V (A)
@@ -140,37 +175,51 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int j = 0; j < 8; ++j) pb[c][j] = (__bf16)s[8 * c + j];
+    const char* vbytes = reinterpret_cast<const char*>(vb);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
+      const int feat = dt * 32 + tr_feat;
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
-        bf16x8 va;
+        bf16x4 v2[2];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int key = 16 * c + 8 * (j >> 2) + 4 * half + (j & 3);
-          va[j] = __builtin_bit_cast(__bf16, sV[key * DH + dt * 32 + col]);
+        for (int i = 0; i < 2; ++i) {
+          const int key = 16 * c + 8 * i + tr_key;
+          const char* pa = vbytes + swz<CPR>(key, feat >> 3) * 16 + (feat & 7) * 2;
+          v2[i] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                 (__attribute__((address_space(3))) i16x4*)pa));
         }
+        const bf16x8 va = __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7);
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[c], o[dt], 0, 0, 0);
       }
     }
+    b ^= 1;
   }
+#undef SURGE_COPY_BLOCK
 
-#undef SURGE_LOAD_KV_BLOCK
   // O^T register r of tile dt: head feature dt*32 + 8*(r/4) + 4*half + r%4
-  // of query q0 + col.
-  if (q0 + col < L) {
-    const float inv = 1.0f / l_run;
-    uint16_t* orow = out + (size_t)(beg + q0 + col) * D + (size_t)h * DH;
+  // of query q0 + col.  Stage the normalised bf16 block in LDS (row =
+  // query), then store whole rows.  All reads of the K/V buffers are done:
+  // their results went into MFMAs.
+  const float inv = 1.0f / l_run;
+  char* obytes = reinterpret_cast<char*>(sO);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
+  for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        uint2 w;
-        w.x = pack_bf16x2(o[dt][4 * g + 0] * inv, o[dt][4 * g + 1] * inv);
-        w.y = pack_bf16x2(o[dt][4 * g + 2] * inv, o[dt][4 * g + 3] * inv);
-        *reinterpret_cast<uint2*>(orow + dt * 32 + 8 * g + 4 * half) = w;
-      }
+    for (int g = 0; g < 4; ++g) {
+      uint2 w;
+      w.x = pack_bf16x2(o[dt][4 * g + 0] * inv, o[dt][4 * g + 1] * inv);
+      w.y = pack_bf16x2(o[dt][4 * g + 2] * inv, o[dt][4 * g + 3] * inv);
+      *reinterpret_cast<uint2*>(obytes + swz<CPR>(col, dt * 4 + g) * 16 + half * 8) = w;
     }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  uint16_t* ob = out + (size_t)(beg + q0) * D + (size_t)h * DH;
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) {
+    const int row = j * RPC + crow;
+    const u32x4 v = sO[j * 64 + lane];
+    if (q0 + row < L)
+      *reinterpret_cast<u32x4*>(ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8) = v;
   }
 }
 

@@ -12,6 +12,7 @@ namespace surge {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -53,6 +54,52 @@ __device__ __forceinline__ uint4 pack8(const float* f) {
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8, u); }
+
+// LDS rows of CPR 16-byte chunks (CPR = 8: 64 bf16, CPR = 4: 32 bf16); the
+// logical chunk c of row r is stored at position c ^ f(r), with
+//   CPR = 8: f(r) = (r & 7) ^ ((r >> 3) & 1),
+//   CPR = 4: f(r) = ((r >> 1) & 3) ^ ((r >> 3) & 1).
+// Reading one logical chunk from 32 consecutive rows, any 8 aligned rows
+// fall on 8 different 16-byte slots of a 128-byte window and any 16 aligned
+// rows on 16 different slots of a 256-byte window: free of bank conflicts
+// whether the LDS serves a 16-byte read 8 lanes at a time over 32 banks or
+// 16 lanes at a time over 64 banks.  Returns the slot index (16-byte units).
+template <int CPR>
+__device__ __forceinline__ int swz(int row, int chunk) {
+  static_assert(CPR == 8 || CPR == 4, "LDS rows of 64 or 32 bf16");
+  if (CPR == 8) return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
+  return row * 4 + (chunk ^ ((row >> 1) & 3) ^ ((row >> 3) & 1));
+}
+
+// A wave copy instruction (below) fills 64 consecutive slots: lane l's slot
+// is row l / CPR (+ 64/CPR per further copy), stored position l % CPR.  The
+// logical chunk that belongs there, the same for every further copy when
+// the copies of a wave start at rows that are multiples of 16:
+//   CPR = 8: (l & 7) ^ (l >> 3) ^ (copy & 1)    (rows 8 apart per copy),
+//   CPR = 4: (l & 3) ^ ((l >> 3) & 3) ^ (l >> 5).
+template <int CPR>
+__device__ __forceinline__ int copy_chunk(int lane, int copy) {
+  if (CPR == 8) return (lane & 7) ^ (lane >> 3) ^ (copy & 1);
+  return (lane & 3) ^ ((lane >> 3) & 3) ^ (lane >> 5);
+}
+
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds):
+// the wave's 64 lanes land contiguously at LDS byte address `lds` (wave
+// uniform, passed in M0).  Inline assembly, so the waits are placed by the
+// kernel itself; the compiler does not track these loads.
+__device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off"
+      :
+      : "v"(g), "s"(lds)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_address(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -42,29 +42,6 @@
 namespace surge {
 namespace {
 
-template <int CPR>
-__device__ __forceinline__ int swz(int row, int chunk) {
-  static_assert(CPR == 8 || CPR == 4, "LDS rows of 64 or 32 bf16");
-  if (CPR == 8) return row * 8 + (chunk ^ (row & 7) ^ ((row >> 3) & 1));
-  return row * 4 + (chunk ^ ((row >> 1) & 3) ^ ((row >> 3) & 1));
-}
-
-// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds):
-// the wave's 64 lanes land contiguously at LDS byte address `lds` (wave
-// uniform, passed in M0).  Issued as inline assembly so that the waits are
-// placed by the kernel itself (s_waitcnt vmcnt before the barrier that
-// publishes a stage); the compiler cannot prove which stage an in-flight
-// copy targets and would otherwise wait for it before every LDS read.
-__device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
-  asm volatile(
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off"
-      :
-      : "v"(g), "s"(lds)
-      : "memory", "m0");
-}
-
 // Wait until at most `later` stages' copies (CPS instructions each) issued
 // after the one needed next are still in flight.  The vector memory counter
 // retires a wave's loads in issue order.
@@ -115,9 +92,6 @@ __device__ __forceinline__ void tile_coords(int b, int n_tiles, int tiles_n, int
   *tm = m_base + grp * 8 + in % rows;
 }
 
-__device__ __forceinline__ uint32_t lds_address(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
 
 template <int BM, int BN, int BK, int NBUF, int WAVES_M, int WAVES_N, int EPI, int ORDER>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) __attribute__((amdgpu_waves_per_eu(2)))
@@ -176,8 +150,7 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   // Its rows are NWAVES * RPC apart.
   constexpr int DSTEP = NWAVES * RPC;
   const int drow = wave * RPC + lane / CPR;
-  const int dch = CPR == 8 ? (lane & 7) ^ (lane >> 3) ^ (wave & 1)
-                           : (lane & 3) ^ ((lane >> 3) & 3) ^ (lane >> 5);
+  const int dch = copy_chunk<CPR>(lane, wave);
   const uint16_t* xg[XI];
 #pragma unroll
   for (int j = 0; j < XI; ++j)
