@@ -195,6 +195,64 @@ surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t
                               float* const* h_part_out, int64_t first_sb, int64_t* n_superbatches,
                               void* hip_stream);
 
+/*
+ * Timing of one streamed encode (surge_encode_all_streamed), from HIP events
+ * on the two streams; milliseconds.  I/O here is the PCIe traffic either
+ * side of the path: the upload of a SuperBatch's tokens and the download of
+ * its embeddings (the GPU analogue of the paper's serialise + upload stage,
+ * Sec. 3.3).
+ */
+typedef struct surge_stream_stats {
+  int64_t n_superbatches;
+  double total_ms;  /* start of the first upload -> end of the last download */
+  double ttfo_ms;   /* start of the first upload -> end of SuperBatch 0's download */
+  double enc_ms;    /* sum over SuperBatches of the encode span */
+  double h2d_ms;    /* sum of the token uploads */
+  double d2h_ms;    /* sum of the embedding downloads */
+  /* I/O overlap ratio of eq. (overlap): 1 - max(0, t_io - t_enc) / t_io with
+   * t_enc and t_io = t_h2d + t_d2h the per-SuperBatch means. */
+  double rho;
+  /* Measured counterpart: 1 - (total_ms - enc_ms) / (h2d_ms + d2h_ms), the
+   * share of the I/O time that did not extend the wall time (clamped to
+   * [0, 1]). */
+  double rho_measured;
+} surge_stream_stats;
+
+/*
+ * Encode a whole partition-grouped input that lives in host memory, as a
+ * stream of SuperBatches (the plan of surge_plan with the same arguments):
+ * SuperBatch j's tokens are uploaded, encoded and its embeddings downloaded
+ * into h_out.  With overlap = 1 the uploads and downloads run on
+ * `copy_stream`, double-buffered, so the download of SuperBatch j and the
+ * upload of j+1 overlap the encode of j+1 on `compute_stream` (Sec. 3.3,
+ * Alg. 2 on the PCIe side of the GPU).  With overlap = 0 everything runs on
+ * `compute_stream` in order (the synchronous baseline).  Returns after both
+ * streams have finished.
+ *
+ * h_token_ids: host int32 [h_cu_seqlens[n_texts]], texts back to back.
+ * h_cu_seqlens: host int64 [n_texts+1], global.  h_part_offsets: host int64
+ *   [n_parts+1]; part_offsets[n_parts] = n_texts.
+ * h_out: host fp32 [n_texts, d_model]; row i is text i's embedding, so
+ *   partition p's E_p is rows part_offsets[p] .. part_offsets[p+1]-1.
+ *   h_token_ids and h_out should be pinned (hipHostMalloc); pageable memory
+ *   works but its copies do not overlap.
+ * copy_stream: a second stream (ignored when overlap = 0); both streams may
+ *   be NULL only when overlap = 0.
+ * h_sb_times: optional [sb_times_cap * 3] doubles; receives (upload, encode,
+ *   download) ms of SuperBatch j at 3j .. 3j+2 for j < sb_times_cap.
+ * stats: optional, receives the timing summary.
+ * The call allocates two token and two embedding staging buffers for the
+ * largest SuperBatch and frees them before returning.  Deferred device
+ * errors (token IDs outside the vocabulary) are reported as by surge_check.
+ */
+surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
+                                       const int32_t* h_token_ids, const int64_t* h_cu_seqlens,
+                                       const int64_t* h_part_offsets, int32_t n_parts,
+                                       int64_t b_min, int64_t n_max, int32_t policy, float* h_out,
+                                       int32_t overlap, void* compute_stream, void* copy_stream,
+                                       double* h_sb_times, int64_t sb_times_cap,
+                                       surge_stream_stats* stats);
+
 /* Synchronise `hip_stream`, then report deferred device-side errors (a token
  * ID outside the vocabulary -> SURGE_ERR_INVALID_ARGUMENT) and clear them. */
 surge_status surge_check(surge_encoder* enc, void* hip_stream);

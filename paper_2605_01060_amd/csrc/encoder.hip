@@ -231,6 +231,30 @@ surge_status check_alignment(int64_t n_segs, const surge_segment* segs, float* c
   return SURGE_OK;
 }
 
+// The SuperBatches of a whole input and their segments (global text
+// indices), from the host planner.
+struct Plan {
+  std::vector<PlanSB> sbs;
+  std::vector<surge_segment> segs;
+};
+
+surge_status make_plan(const int64_t* part_offsets, int32_t n_parts, int64_t b_min, int64_t n_max,
+                       int32_t policy, Plan* plan, int64_t* n_sbs) {
+  auto on_sb = [](void* c, const PlanSB& s) { ((Plan*)c)->sbs.push_back(s); };
+  auto on_seg = [](void* c, const PlanSeg& s) {
+    surge_segment g;
+    g.first_text = s.first_text;
+    g.count = s.count;
+    g.row_offset = s.row_offset;
+    g.partition = s.partition;
+    g.reserved = 0;
+    ((Plan*)c)->segs.push_back(g);
+  };
+  int64_t ng = 0;
+  return plan_superbatches(part_offsets, n_parts, b_min, n_max, policy, on_sb, on_seg, plan, n_sbs,
+                           &ng);
+}
+
 }  // namespace
 
 extern "C" {
@@ -457,23 +481,9 @@ surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t
   if (n_parts < 0 || h_part_offsets[n_parts] != n_texts)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts] != n_texts");
   if (first_sb < 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "first_sb < 0");
-  struct Ctx {
-    std::vector<PlanSB> sbs;
-    std::vector<surge_segment> segs;
-  } ctx;
-  auto on_sb = [](void* c, const PlanSB& s) { ((Ctx*)c)->sbs.push_back(s); };
-  auto on_seg = [](void* c, const PlanSeg& s) {
-    surge_segment g;
-    g.first_text = s.first_text;
-    g.count = s.count;
-    g.row_offset = s.row_offset;
-    g.partition = s.partition;
-    g.reserved = 0;
-    ((Ctx*)c)->segs.push_back(g);
-  };
-  int64_t ns = 0, ng = 0;
-  surge_status st = plan_superbatches(h_part_offsets, n_parts, b_min, n_max, policy, on_sb, on_seg,
-                                      &ctx, &ns, &ng);
+  Plan ctx;
+  int64_t ns = 0;
+  surge_status st = make_plan(h_part_offsets, n_parts, b_min, n_max, policy, &ctx, &ns);
   if (st != SURGE_OK) return st;
   if (n_superbatches) *n_superbatches = ns;
   // Validate the whole input once, then every SuperBatch is consistent.
@@ -507,6 +517,184 @@ surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t
     }
     st = encode_chunks(e, S, d_token_ids + base, lcu.data(), (hipStream_t)hip_stream);
     if (st != SURGE_OK) return st;
+  }
+  return SURGE_OK;
+}
+
+surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
+                                       const int32_t* h_token_ids, const int64_t* h_cu_seqlens,
+                                       const int64_t* h_part_offsets, int32_t n_parts,
+                                       int64_t b_min, int64_t n_max, int32_t policy, float* h_out,
+                                       int32_t overlap, void* compute_stream, void* copy_stream,
+                                       double* h_sb_times, int64_t sb_times_cap,
+                                       surge_stream_stats* stats) {
+  clear_error();
+  if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
+  if (!h_part_offsets || !h_cu_seqlens) return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL host array");
+  if (n_parts < 0 || h_part_offsets[n_parts] != n_texts)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts] != n_texts");
+  if (overlap != 0 && overlap != 1) return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap=%d", overlap);
+  if (overlap && compute_stream == copy_stream)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap needs two different streams");
+  if (h_sb_times == nullptr && sb_times_cap != 0)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "sb_times_cap > 0 with NULL h_sb_times");
+  Plan plan;
+  int64_t ns = 0;
+  surge_status st = make_plan(h_part_offsets, n_parts, b_min, n_max, policy, &plan, &ns);
+  if (st != SURGE_OK) return st;
+  const int64_t d = enc->desc.d_model;
+  // Validate once against per-partition views of h_out (never dereferenced).
+  std::vector<int64_t> sizes((size_t)n_parts);
+  std::vector<float*> views((size_t)n_parts);
+  for (int32_t p = 0; p < n_parts; ++p) {
+    sizes[p] = h_part_offsets[p + 1] - h_part_offsets[p];
+    views[p] = h_out ? h_out + h_part_offsets[p] * d : nullptr;
+  }
+  st = surge_validate_superbatch(&enc->desc, n_texts, h_cu_seqlens[n_texts], h_cu_seqlens,
+                                 plan.segs.data(), (int64_t)plan.segs.size(), sizes.data(),
+                                 views.data(), n_parts);
+  if (st != SURGE_OK) return st;
+  if (stats) memset(stats, 0, sizeof(*stats));
+  if (n_texts == 0) return SURGE_OK;
+  if (!h_token_ids) return fail(SURGE_ERR_INVALID_ARGUMENT, "token_ids is NULL");
+  if (((uintptr_t)h_out) & 15u) return fail(SURGE_ERR_INVALID_ARGUMENT, "h_out is not 16-byte aligned");
+  HIP_TRY(hipSetDevice(enc->device));
+  surge_encoder* e = enc;
+  hipStream_t cs = (hipStream_t)compute_stream;
+  hipStream_t xs = overlap ? (hipStream_t)copy_stream : cs;
+
+  int64_t max_tok = 0, max_txt = 0;
+  for (const PlanSB& sb : plan.sbs) {
+    max_tok = std::max(max_tok, h_cu_seqlens[sb.text_end] - h_cu_seqlens[sb.text_begin]);
+    max_txt = std::max(max_txt, sb.text_end - sb.text_begin);
+  }
+  // Staging buffers and events, released on every exit path after both
+  // streams have drained.
+  struct Res {
+    int32_t* tok[2] = {nullptr, nullptr};
+    float* out[2] = {nullptr, nullptr};
+    std::vector<hipEvent_t> ev;
+    hipStream_t s1 = nullptr, s2 = nullptr;
+    ~Res() {
+      if (s1) hipStreamSynchronize(s1);
+      if (s2) hipStreamSynchronize(s2);
+      for (int i = 0; i < 2; ++i) {
+        if (tok[i]) hipFree(tok[i]);
+        if (out[i]) hipFree(out[i]);
+      }
+      for (hipEvent_t x : ev) hipEventDestroy(x);
+    }
+  } r;
+  r.s1 = cs;
+  r.s2 = xs;
+  for (int i = 0; i < 2; ++i) {
+    HIP_TRY(hipMalloc(&r.tok[i], (size_t)std::max<int64_t>(max_tok, 1) * 4));
+    HIP_TRY(hipMalloc(&r.out[i], (size_t)max_txt * d * 4));
+  }
+  // Six events per SuperBatch: upload, encode and download start / end.
+  r.ev.resize((size_t)ns * 6, nullptr);
+  for (hipEvent_t& x : r.ev) HIP_TRY(hipEventCreate(&x));
+  auto EV = [&](int64_t j, int k) { return r.ev[(size_t)j * 6 + k]; };
+  enum { H2D0, H2D1, ENC0, ENC1, D2H0, D2H1 };
+
+  auto upload = [&](int64_t j) -> surge_status {
+    const PlanSB& sb = plan.sbs[(size_t)j];
+    const int64_t t0 = h_cu_seqlens[sb.text_begin], t1 = h_cu_seqlens[sb.text_end];
+    HIP_TRY(hipEventRecord(EV(j, H2D0), xs));
+    HIP_TRY(hipMemcpyAsync(r.tok[j & 1], h_token_ids + t0, (size_t)(t1 - t0) * 4,
+                           hipMemcpyHostToDevice, xs));
+    HIP_TRY(hipEventRecord(EV(j, H2D1), xs));
+    return SURGE_OK;
+  };
+  auto download = [&](int64_t j) -> surge_status {
+    const PlanSB& sb = plan.sbs[(size_t)j];
+    const int64_t S = sb.text_end - sb.text_begin;
+    HIP_TRY(hipEventRecord(EV(j, D2H0), xs));
+    HIP_TRY(hipMemcpyAsync(h_out + sb.text_begin * d, r.out[j & 1], (size_t)S * d * 4,
+                           hipMemcpyDeviceToHost, xs));
+    HIP_TRY(hipEventRecord(EV(j, D2H1), xs));
+    return SURGE_OK;
+  };
+  std::vector<int64_t> lcu;
+  st = upload(0);
+  if (st != SURGE_OK) return st;
+  for (int64_t j = 0; j < ns; ++j) {
+    const PlanSB& sb = plan.sbs[(size_t)j];
+    const int64_t S = sb.text_end - sb.text_begin;
+    if (overlap) {
+      HIP_TRY(hipStreamWaitEvent(cs, EV(j, H2D1), 0));
+      if (j >= 2) HIP_TRY(hipStreamWaitEvent(cs, EV(j - 2, D2H1), 0));  // staging j&1 is free
+    }
+    // Rows of this SuperBatch's texts in the embedding staging buffer.
+    e->h_dst.resize((size_t)S);
+    for (int64_t i = 0; i < S; ++i)
+      e->h_dst[(size_t)i] = (uint64_t)(uintptr_t)(r.out[j & 1] + i * d);
+    lcu.resize((size_t)S + 1);
+    const int64_t base = h_cu_seqlens[sb.text_begin];
+    for (int64_t i = 0; i <= S; ++i) lcu[(size_t)i] = h_cu_seqlens[sb.text_begin + i] - base;
+    HIP_TRY(hipEventRecord(EV(j, ENC0), cs));
+    st = encode_chunks(e, S, r.tok[j & 1], lcu.data(), cs);
+    if (st != SURGE_OK) return st;
+    HIP_TRY(hipEventRecord(EV(j, ENC1), cs));
+    if (overlap) {
+      if (j + 1 < ns) {
+        if (j >= 1) HIP_TRY(hipStreamWaitEvent(xs, EV(j - 1, ENC1), 0));  // tokens j+1 & 1 free
+        st = upload(j + 1);
+        if (st != SURGE_OK) return st;
+      }
+      HIP_TRY(hipStreamWaitEvent(xs, EV(j, ENC1), 0));
+      st = download(j);
+      if (st != SURGE_OK) return st;
+    } else {
+      st = download(j);
+      if (st != SURGE_OK) return st;
+      if (j + 1 < ns) {
+        st = upload(j + 1);
+        if (st != SURGE_OK) return st;
+      }
+    }
+  }
+  HIP_TRY(hipStreamSynchronize(cs));
+  HIP_TRY(hipStreamSynchronize(xs));
+  // Timing summary.
+  auto span = [&](hipEvent_t a, hipEvent_t b) {
+    float ms = 0.0f;
+    hipEventElapsedTime(&ms, a, b);
+    return (double)ms;
+  };
+  double enc_ms = 0.0, h2d_ms = 0.0, d2h_ms = 0.0;
+  for (int64_t j = 0; j < ns; ++j) {
+    const double u = span(EV(j, H2D0), EV(j, H2D1));
+    const double c = span(EV(j, ENC0), EV(j, ENC1));
+    const double w = span(EV(j, D2H0), EV(j, D2H1));
+    h2d_ms += u;
+    enc_ms += c;
+    d2h_ms += w;
+    if (j < sb_times_cap) {
+      h_sb_times[3 * j + 0] = u;
+      h_sb_times[3 * j + 1] = c;
+      h_sb_times[3 * j + 2] = w;
+    }
+  }
+  if (stats) {
+    stats->n_superbatches = ns;
+    stats->total_ms = span(EV(0, H2D0), EV(ns - 1, D2H1));
+    stats->ttfo_ms = span(EV(0, H2D0), EV(0, D2H1));
+    stats->enc_ms = enc_ms;
+    stats->h2d_ms = h2d_ms;
+    stats->d2h_ms = d2h_ms;
+    const double io = (h2d_ms + d2h_ms) / (double)ns, ce = enc_ms / (double)ns;
+    stats->rho = io > 0.0 ? 1.0 - std::max(0.0, io - ce) / io : 1.0;
+    const double exposed = stats->total_ms - enc_ms;
+    stats->rho_measured =
+        h2d_ms + d2h_ms > 0.0 ? std::min(1.0, std::max(0.0, 1.0 - exposed / (h2d_ms + d2h_ms)))
+                              : 1.0;
+  }
+  int flag = 0;
+  HIP_TRY(hipMemcpy(&flag, e->d_err, sizeof(int), hipMemcpyDeviceToHost));
+  if (flag) {
+    HIP_TRY(hipMemset(e->d_err, 0, sizeof(int)));
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "a token ID outside [0, vocab) was encoded as ID 0");
   }
   return SURGE_OK;
 }

@@ -48,6 +48,13 @@ class EncoderDesc(ctypes.Structure):
                 ("ln_eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
 
 
+class StreamStats(ctypes.Structure):
+    _fields_ = [("n_superbatches", ctypes.c_int64), ("total_ms", ctypes.c_double),
+                ("ttfo_ms", ctypes.c_double), ("enc_ms", ctypes.c_double),
+                ("h2d_ms", ctypes.c_double), ("d2h_ms", ctypes.c_double),
+                ("rho", ctypes.c_double), ("rho_measured", ctypes.c_double)]
+
+
 class KernelStat(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int64), ("total_ms", ctypes.c_double),
                 ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
@@ -69,6 +76,8 @@ _SIGNATURES = {
     "surge_encoder_info": ([_P, _P, _P, _P], _I32),
     "surge_encode_superbatch": ([_P, _I64, _I64, _P, _P, _P, _I64, _P, _P, _I32, _P], _I32),
     "surge_encode_all": ([_P, _I64, _P, _P, _P, _I32, _I64, _I64, _I32, _P, _I64, _P, _P], _I32),
+    "surge_encode_all_streamed": ([_P, _I64, _P, _P, _P, _I32, _I64, _I64, _I32, _P, _I32, _P, _P,
+                                   _P, _I64, _P], _I32),
     "surge_check": ([_P, _P], _I32),
     "surge_profile_enable": ([_P, _I32], _I32),
     "surge_profile_read": ([_P, _P, _I32], _I32),
@@ -115,6 +124,19 @@ def _dev(x) -> int:
         return 0
     if isinstance(x, int):
         return x
+    return int(x.data_ptr())
+
+
+def _hptr(x) -> int:
+    """Address of a host buffer: a NumPy array or a CPU torch tensor."""
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if isinstance(x, np.ndarray):
+        assert x.flags.c_contiguous
+        return x.ctypes.data
+    assert not x.is_cuda and x.is_contiguous()
     return int(x.data_ptr())
 
 
@@ -219,6 +241,28 @@ def surge_encode_all(handle: int, n_texts: int, d_token_ids, cu_seqlens, part_of
     return nsb.value
 
 
+
+def surge_encode_all_streamed(handle: int, n_texts: int, h_token_ids, cu_seqlens, part_offsets,
+                              b_min: int, n_max: int, policy: int, h_out, overlap: int,
+                              compute_stream=None, copy_stream=None,
+                              sb_times: Optional[np.ndarray] = None) -> Dict[str, float]:
+    """h_token_ids / h_out: host buffers (pinned torch CPU tensors or NumPy
+    arrays; pass pinned memory for overlapping copies).  Returns the timing
+    summary; per-SuperBatch (upload, encode, download) ms go to sb_times
+    [cap, 3] float64 if given."""
+    cu, pcu = _host(cu_seqlens, np.int64)
+    offs, poff = _host(part_offsets, np.int64)
+    st = StreamStats()
+    cap = 0 if sb_times is None else int(sb_times.shape[0])
+    pt = 0 if sb_times is None else sb_times.ctypes.data
+    if sb_times is not None:
+        assert sb_times.dtype == np.float64 and sb_times.flags.c_contiguous and sb_times.shape[1:] == (3,)
+    _check(lib().surge_encode_all_streamed(handle, n_texts, _hptr(h_token_ids), pcu, poff,
+                                           offs.shape[0] - 1, b_min, n_max, policy, _hptr(h_out),
+                                           overlap, _stream(compute_stream), _stream(copy_stream),
+                                           pt, cap, ctypes.byref(st)))
+    return {k: getattr(st, k) for k, _ in StreamStats._fields_}
+
 def surge_check(handle: int, stream=None):
     _check(lib().surge_check(handle, _stream(stream)))
 
@@ -291,6 +335,13 @@ class Encoder:
                    part_out_ptrs, policy=SURGE_POLICY_SPLIT, first_sb=0, stream=None) -> int:
         return surge_encode_all(self.handle, n_texts, d_tokens, cu_seqlens, part_offsets, b_min,
                                 n_max, policy, part_out_ptrs, first_sb, stream)
+
+    def encode_all_streamed(self, n_texts, h_tokens, cu_seqlens, part_offsets, b_min, n_max,
+                            h_out, overlap=1, compute_stream=None, copy_stream=None,
+                            policy=SURGE_POLICY_SPLIT, sb_times=None) -> Dict[str, float]:
+        return surge_encode_all_streamed(self.handle, n_texts, h_tokens, cu_seqlens, part_offsets,
+                                         b_min, n_max, policy, h_out, overlap, compute_stream,
+                                         copy_stream, sb_times)
 
     def encode_superbatch(self, n_texts, n_tokens, d_tokens, cu_seqlens, segments,
                           part_out_ptrs, part_sizes, stream=None):
