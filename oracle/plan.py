@@ -137,3 +137,36 @@ def flatten(sbs: List[SuperBatch]) -> Tuple[List[Tuple[int, int, int, int]],
             seg_rows.append((s.first_text, s.count, s.partition, s.row_offset))
         sb_rows.append((sb.text_begin, sb.text_end, s0, len(seg_rows)))
     return sb_rows, seg_rows
+
+
+# --- Cost model (Sec. 2.3 and Theorem 1) ---------------------------------
+#
+# A call that encodes n texts on G GPUs costs c_call + n c_enc / G: a fixed
+# per-call overhead plus a per-text cost shared by the GPUs.  A plan with F
+# calls over N texts therefore takes F c_call + N c_enc / G.
+
+def call_time(n_texts: int, c_call: float, c_enc: float, n_gpus: int = 1) -> float:
+    """Time of one encode call of n_texts texts (Sec. 2.3)."""
+    return c_call + n_texts * c_enc / n_gpus
+
+
+def plan_time(call_sizes: Sequence[int], c_call: float, c_enc: float, n_gpus: int = 1) -> float:
+    """Sum of the call times of a plan."""
+    return float(sum(call_time(n, c_call, c_enc, n_gpus) for n in call_sizes))
+
+
+def ipc_alpha(n_parts: int, c_call: float, n_texts: int, c_enc: float, n_gpus: int = 1) -> float:
+    """Theorem 1's IPC-to-compute ratio of one-call-per-partition processing."""
+    return n_parts * c_call / (n_texts * c_enc / n_gpus)
+
+
+def ipc_speedup(alpha: float, n_flushes: int, n_parts: int) -> float:
+    """Theorem 1: T_PBP / T_SURGE when PBP makes n_parts calls and SURGE
+    n_flushes calls over the same texts."""
+    return (1.0 + alpha) / (1.0 + alpha * n_flushes / n_parts)
+
+
+def ipc_threshold(c_call: float, c_enc: float, n_gpus: int = 1) -> float:
+    """n*: partitions smaller than this spend more time on the fixed call
+    overhead than on encoding (Sec. 2.3)."""
+    return c_call * n_gpus / c_enc
