@@ -170,3 +170,38 @@ def ipc_threshold(c_call: float, c_enc: float, n_gpus: int = 1) -> float:
     """n*: partitions smaller than this spend more time on the fixed call
     overhead than on encoding (Sec. 2.3)."""
     return c_call * n_gpus / c_enc
+
+
+# --- PB-PBP-LB baseline (Sec. 5.x "stronger baseline") --------------------
+#
+# Partition sizes are known up front; partitions are taken largest first
+# (ties: lower index first) and each goes into the first open batch whose
+# remaining capacity holds it, else into a new batch.  Partitions are never
+# split, so a partition larger than the capacity forms a batch of its own.
+
+def ffd_pack(part_sizes: Sequence[int], capacity: int) -> List[List[int]]:
+    """First-Fit-Decreasing batches (lists of partition indices, in packing
+    order) of the non-empty partitions."""
+    if capacity < 1:
+        raise ValueError("capacity must be >= 1")
+    order = sorted((p for p, n in enumerate(part_sizes) if n > 0),
+                   key=lambda p: (-part_sizes[p], p))
+    bins: List[List[int]] = []
+    load: List[int] = []
+    for p in order:
+        n = part_sizes[p]
+        for b in range(len(bins)):
+            if load[b] + n <= capacity:
+                bins[b].append(p)
+                load[b] += n
+                break
+        else:
+            bins.append([p])
+            load.append(n)
+    return bins
+
+
+def superbatch_memory(n_texts: int, n_tokens: int, d: int, bytes_per_token: int = 4) -> int:
+    """Lemma 1's data-resident size of a SuperBatch, M(S) = S L + 4 S d bytes,
+    with the text part counted as its token IDs (bytes_per_token each)."""
+    return n_tokens * bytes_per_token + 4 * n_texts * d

@@ -101,3 +101,119 @@ def test_fit_call_cost_recovers_line():
     ms = 1.75 + n * 0.0123
     c0, c1 = CC.fit_call_cost(n, ms)
     assert c0 == pytest.approx(1.75, rel=1e-9) and c1 == pytest.approx(0.0123, rel=1e-9)
+
+
+# --- PB-PBP-LB (FFD) and Lemma 1 -------------------------------------------
+
+FFD_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "ffd_cases.json")
+
+
+def test_ffd_golden():
+    for c in json.load(open(FFD_GOLDEN))["cases"]:
+        assert OP.ffd_pack(c["sizes"], c["capacity"]) == c["batches"]
+        assert CC.ffd_batches(c["sizes"], c["capacity"]) == c["batches"]
+
+
+def _opt_bins(sizes, cap):
+    """Fewest bins by exhaustive search (tiny inputs)."""
+    items = sorted([s for s in sizes if s > 0], reverse=True)
+    best = [len(items)]
+
+    def rec(i, loads):
+        if len(loads) >= best[0]:
+            return
+        if i == len(items):
+            best[0] = len(loads)
+            return
+        seen = set()
+        for b in range(len(loads)):
+            if loads[b] + items[i] <= cap and loads[b] not in seen:
+                seen.add(loads[b])
+                loads[b] += items[i]
+                rec(i + 1, loads)
+                loads[b] -= items[i]
+        loads.append(items[i])
+        rec(i + 1, loads)
+        loads.pop()
+
+    rec(0, [])
+    return best[0]
+
+
+@settings(max_examples=150, deadline=None)
+@given(st.lists(st.integers(0, 10), min_size=1, max_size=9), st.integers(10, 14))
+def test_ffd_invariants_and_bound(sizes, cap):
+    bins = OP.ffd_pack(sizes, cap)
+    flat = sorted(p for b in bins for p in b)
+    assert flat == [p for p, n in enumerate(sizes) if n > 0]  # every partition once, whole
+    assert all(sum(sizes[p] for p in b) <= cap for b in bins)
+    # the FFD guarantee (Dósa 2007): FFD <= 11/9 OPT + 6/9
+    opt = _opt_bins(sizes, cap)
+    assert len(bins) <= 11 / 9 * opt + 6 / 9 + 1e-9
+    assert CC.ffd_batches(sizes, cap) == bins
+
+
+def test_ffd_oversized_partition_alone():
+    bins = OP.ffd_pack([3, 25, 4, 30], 10)
+    assert bins[0] == [3] and bins[1] == [1]  # never split, one batch each
+    assert CC.ffd_batches([3, 25, 4, 30], 10) == bins
+
+
+def test_plan_ffd_layout():
+    wl = W.make_workload(W.WORKLOADS["minilm"])
+    calls, perm, cu = CC.plan_ffd(wl.part_offsets, wl.cu_seqlens, 3000)
+    assert sorted(perm.tolist()) == list(range(wl.n_texts))
+    assert cu[-1] == wl.n_tokens
+    lens = np.diff(wl.cu_seqlens)
+    assert np.array_equal(np.diff(cu), lens[perm])
+    for t0, t1, segs in calls:
+        for s in segs:
+            p = int(s["partition"])
+            assert s["row_offset"] == 0 and s["count"] == wl.part_offsets[p + 1] - wl.part_offsets[p]
+            a = t0 + int(s["first_text"])
+            assert np.array_equal(perm[a:a + int(s["count"])],
+                                  np.arange(wl.part_offsets[p], wl.part_offsets[p + 1]))
+    tp = CC.permuted_tokens(wl.tokens, wl.cu_seqlens, perm)
+    for k in (0, 17, wl.n_texts - 1):
+        t = perm[k]
+        assert np.array_equal(tp[cu[k]:cu[k + 1]], wl.tokens[wl.cu_seqlens[t]:wl.cu_seqlens[t + 1]])
+
+
+def test_adversarial_order():
+    sizes = np.array([50, 3, 900, 7, 2, 40, 5])
+    order = CC.adversarial_order(sizes, 20)
+    assert sorted(order.tolist()) == list(range(sizes.size))
+    k = order.tolist().index(2)
+    assert sizes[order[:k]].sum() < 20 and k > 0  # a buffer just short of B_min, then the largest
+    assert OP.plan([0] + np.cumsum(sizes[order]).tolist(), 20, 0, OP.R1)[0].n_texts == \
+        sizes[order[:k + 1]].sum()
+
+
+@settings(max_examples=100, deadline=None)
+@given(st.lists(st.integers(0, 400), min_size=1, max_size=40), st.integers(1, 300),
+       st.integers(1, 600))
+def test_lemma1_bound(sizes, b_min, cap):
+    """Largest SuperBatch: R1 <= (B_min - 1) + n_max, R2 <= cap; both in
+    every arrival order, including the adversarial one."""
+    sizes = np.array(sizes)
+    n_big = int(sizes.max())
+    for order in (np.arange(sizes.size), CC.adversarial_order(sizes, b_min)):
+        offs = [0] + np.cumsum(sizes[order]).tolist()
+        r1 = max([sb.n_texts for sb in OP.plan(offs, b_min, 0, OP.R1)] + [0])
+        r2 = max([sb.n_texts for sb in OP.plan(offs, b_min, cap, OP.R2)] + [0])
+        assert r1 <= b_min - 1 + n_big
+        assert r2 <= cap
+
+
+def test_lemma1_table_heavy():
+    spec = W.WORKLOADS["minilm_heavy"]
+    wl = W.make_workload(spec)
+    rows = CC.lemma1_table(wl, spec.b_min, spec.n_max, spec.encoder.d_model)
+    assert all(r["within_bound"] for r in rows)
+    r2 = [r for r in rows if r["plan"] == "R2"]
+    r1 = [r for r in rows if r["plan"] == "R1"]
+    assert all(r["max_texts"] <= spec.n_max for r in r2)
+    # without the cap a single oversized partition drives the largest call
+    assert all(r["max_texts"] > 10 * spec.n_max for r in r1)
+    m = OP.superbatch_memory(10, 100, 384)
+    assert m == 100 * 4 + 4 * 10 * 384

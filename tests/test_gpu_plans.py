@@ -1,6 +1,7 @@
 """The same texts encoded under the three plans of the cost-model
 comparison (one call per partition, fixed chunks across partition
-boundaries, SURGE SuperBatches) give bit-identical rows: a text's result
+boundaries, SURGE SuperBatches, FFD-packed whole partitions) give
+bit-identical rows: a text's result
 does not depend on which call it rides in (the premise of Sec. 2.2's
 comparison), and every row lands in its partition's segment.
 """
@@ -36,7 +37,14 @@ def test_plans_bit_identical():
         print(f"[plans] {name}: {r['calls']} calls, {r['total_ms']:.2f} ms", flush=True)
         assert r["calls"] == len(calls) and np.all(r["call_ms"] > 0)
         outs[name] = out.cpu().numpy()
+    # PB-PBP-LB: FFD batches of whole partitions, texts re-laid out batch by batch
+    calls, perm, cu = CC.plan_ffd(wl.part_offsets, wl.cu_seqlens, 2500)
+    tok_ffd = torch.from_numpy(CC.permuted_tokens(wl.tokens, wl.cu_seqlens, perm)).cuda()
+    out = torch.full((wl.n_texts, sh.d_model), float("nan"), device="cuda")
+    r = CC.run_calls(torch, enc, wl, calls, tok_ffd, out, stream, cu=cu)
+    print(f"[plans] ffd: {r['calls']} calls, {r['total_ms']:.2f} ms", flush=True)
+    outs["ffd"] = out.cpu().numpy()
     assert not np.isnan(outs["surge"]).any()
-    np.testing.assert_array_equal(outs["pbp"], outs["surge"])
-    np.testing.assert_array_equal(outs["fsb"], outs["surge"])
+    for name in ("pbp", "fsb", "ffd"):
+        np.testing.assert_array_equal(outs[name], outs["surge"])
     enc.close()
