@@ -45,6 +45,36 @@ surge_status surge_op_linear(int64_t M, int32_t N, int32_t K, const uint16_t* d_
                              int32_t epilogue, uint16_t* d_y, void* hip_stream);
 
 /*
+ * The linear layer's LayerNorm-fused forms (post-LN encoder with every
+ * LayerNorm except the last folded into its neighbours; LN(v) = gamma (v -
+ * mu) / sqrt(var + eps) + beta over a row, biased variance):
+ *   epilogue 3: y = LN(x) W^T + b for raw rows x of d_x, computed as
+ *               rstd (x W'^T - mu s) + b' with d_w = W' = bf16(W diag(gamma)),
+ *               d_col_s = s = row sums of W' [N] and d_bias = b' = b + W beta;
+ *               the row statistics of x come from d_stats_in;
+ *   epilogue 4: epilogue 3, then exact GELU;
+ *   epilogue 5: y = x W^T + b + res, and the statistics of y's rows are
+ *               written to d_stats_out;
+ *   epilogue 6: y = x W^T + b + LN(res) with res's statistics in d_stats_in
+ *               and LN's gamma, beta in d_gamma, d_beta [N]; statistics of y
+ *               to d_stats_out.
+ *   epilogues 0-2 as surge_op_linear.
+ * Statistics are partials of W = surge_op_linear_stats_width(M, N)
+ * consecutive features of a row: fp32 pairs (mean, variance) at
+ * [(p * M + row) * 2], p < N / W.  d_stats_in holds parts_in partials of
+ * equal width per row (the producer's N / W).  Shapes as surge_op_linear;
+ * float vectors 16-byte aligned.
+ */
+surge_status surge_op_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                                const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
+                                int32_t epilogue, const float* d_stats_in, int32_t parts_in,
+                                const float* d_col_s, const float* d_gamma, const float* d_beta,
+                                float eps, float* d_stats_out, uint16_t* d_y, void* hip_stream);
+
+/* Features per statistics partial of an [M, N] linear output (host-only). */
+int32_t surge_op_linear_stats_width(int64_t M, int32_t N);
+
+/*
  * Packed varlen multi-head self-attention within each text:
  * out[rows of text i, head h] = softmax(Q_h K_h^T / sqrt(d_head)) V_h.
  * d_qkv bf16 [T, 3 n_heads d_head] (Q | K | V blocks, head h at columns

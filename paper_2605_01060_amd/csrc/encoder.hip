@@ -32,6 +32,10 @@ constexpr int kStagingSlots = 4;
 struct LayerWeights {
   uint16_t *wqkv, *wo, *w1, *w2;               // bf16 [out, in]
   float *bqkv, *bo, *ln1g, *ln1b, *b1, *b2, *ln2g, *ln2b;  // fp32
+  // The LayerNorm before the QKV (layers >= 1: the previous layer's LN2) and
+  // before FFN1 (LN1) is folded into those GEMMs: W' = W diag(gamma) is what
+  // wqkv / w1 hold, s = row sums of W', and bqkv / b1 hold b + W beta.
+  float *sqkv, *s1;                            // fp32 [3d], [d_ff]
 };
 
 struct ProfRecord {
@@ -55,6 +59,8 @@ struct surge_encoder {
   void* wsblock = nullptr;
   int64_t ws_bytes = 0;
   uint16_t *X = nullptr, *QKV = nullptr, *CTX = nullptr, *Y = nullptr, *H = nullptr;
+  float2 *SX = nullptr, *SY = nullptr;  // row statistics partials of X and Y
+  float2 *RX = nullptr, *RY = nullptr;  // their per-row LayerNorm factors
   int32_t* d_cu = nullptr;     // [max_tokens + 1]
   uint64_t* d_dst = nullptr;   // [max_tokens]
   uint32_t* d_items = nullptr; // [max_tokens] attention work items
@@ -186,25 +192,53 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
     LAUNCH(SURGE_KERNEL_EMBED, 0.0, Td * (4.0 + 6.0 * d),
            launch_embed_ln(toks, e->d_cu, Si, e->word, e->pos, e->lneg, e->lneb, D.ln_eps,
                            D.vocab_size, d, e->X, e->d_err, stream));
+    // Post-LN with the LayerNorms folded into their neighbours: X and Y
+    // hold raw (pre-LN) residual rows, SX and SY their statistics partials
+    // (written by the residual GEMMs), RX and RY the per-row factors.
+    const int parts = d / linear_stats_width(T, d);  // partials of a [T, d] output
     for (int l = 0; l < D.n_layers; ++l) {
       const LayerWeights& w = e->layers[l];
+      const LayerWeights* pw = l > 0 ? &e->layers[l - 1] : nullptr;
+      LinearExtra xq;  // QKV: LN2 of the previous layer folded in (layer 0: plain)
+      xq.rows_in = e->RX;
+      xq.col_s = w.sqkv;
       LAUNCH(SURGE_KERNEL_QKV, 2.0 * Td * d * 3 * d, 2.0 * (Td * d + 3.0 * d * d + Td * 3 * d),
-             launch_linear(e->X, w.wqkv, w.bqkv, nullptr, e->QKV, T, 3 * d, d, EPI_BIAS, stream));
+             launch_linear(e->X, w.wqkv, w.bqkv, nullptr, e->QKV, T, 3 * d, d,
+                           l == 0 ? EPI_BIAS : EPI_FOLD, xq, stream));
       LAUNCH(SURGE_KERNEL_ATTN, 4.0 * d * sumL2, 2.0 * Td * 4 * d,
              launch_attention(e->QKV, e->CTX, e->d_cu, e->d_items, n_items, D.n_heads, dh, stream));
+      LinearExtra xo;  // O-proj + residual (LN2 of the previous layer applied to it)
+      xo.rows_in = e->RX;
+      xo.stats_out = e->SY;
+      xo.gamma = pw ? pw->ln2g : nullptr;
+      xo.beta = pw ? pw->ln2b : nullptr;
       LAUNCH(SURGE_KERNEL_OPROJ, 2.0 * Td * d * d, 2.0 * (3.0 * Td * d + (double)d * d),
-             launch_linear(e->CTX, w.wo, w.bo, e->X, e->Y, T, d, d, EPI_BIAS_RESIDUAL, stream));
-      LAUNCH(SURGE_KERNEL_LN1, 0.0, 4.0 * Td * d,
-             launch_layernorm(e->Y, w.ln1g, w.ln1b, D.ln_eps, e->X, T, d, stream));
+             launch_linear(e->CTX, w.wo, w.bo, e->X, e->Y, T, d, d,
+                           l == 0 ? EPI_RES_STATS : EPI_LNRES_STATS, xo, stream));
+      LAUNCH(SURGE_KERNEL_LN1, 0.0, Td * (8.0 * parts + 8.0),
+             launch_ln_rows(e->SY, parts, T, D.ln_eps, e->RY, stream));
+      LinearExtra x1;  // FFN1: LN1 folded in
+      x1.rows_in = e->RY;
+      x1.col_s = w.s1;
       LAUNCH(SURGE_KERNEL_FFN1, 2.0 * Td * d * f, 2.0 * (Td * d + (double)d * f + Td * f),
-             launch_linear(e->X, w.w1, w.b1, nullptr, e->H, T, f, d, EPI_BIAS_GELU, stream));
+             launch_linear(e->Y, w.w1, w.b1, nullptr, e->H, T, f, d, EPI_FOLD_GELU, x1, stream));
+      LinearExtra x2;  // FFN2 + residual LN1(Y)
+      x2.rows_in = e->RY;
+      x2.stats_out = e->SX;
+      x2.gamma = w.ln1g;
+      x2.beta = w.ln1b;
       LAUNCH(SURGE_KERNEL_FFN2, 2.0 * Td * d * f, 2.0 * (Td * f + (double)d * f + 2.0 * Td * d),
-             launch_linear(e->H, w.w2, w.b2, e->X, e->Y, T, d, f, EPI_BIAS_RESIDUAL, stream));
-      LAUNCH(SURGE_KERNEL_LN2, 0.0, 4.0 * Td * d,
-             launch_layernorm(e->Y, w.ln2g, w.ln2b, D.ln_eps, e->X, T, d, stream));
+             launch_linear(e->H, w.w2, w.b2, e->Y, e->X, T, d, f, EPI_LNRES_STATS, x2, stream));
+      if (l + 1 < D.n_layers)  // the last layer's LN2 is applied below
+        LAUNCH(SURGE_KERNEL_LN2, 0.0, Td * (8.0 * parts + 8.0),
+               launch_ln_rows(e->SX, parts, T, D.ln_eps, e->RX, stream));
     }
+    // The last layer's LN2, materialised once for pooling.
+    const LayerWeights& wl = e->layers[D.n_layers - 1];
+    LAUNCH(SURGE_KERNEL_LN2, 0.0, 4.0 * Td * d,
+           launch_layernorm(e->X, wl.ln2g, wl.ln2b, D.ln_eps, e->Y, T, d, stream));
     LAUNCH(SURGE_KERNEL_POOL, 0.0, 2.0 * Td * d + 4.0 * S * d,
-           launch_pool_l2_scatter(e->X, e->d_cu, Si, e->d_dst, d, stream));
+           launch_pool_l2_scatter(e->Y, e->d_cu, Si, e->d_dst, d, stream));
     t0 = t1;
   }
   return SURGE_OK;
@@ -317,6 +351,11 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
     take((size_t)d * 4);          // ln2g
     take((size_t)d * 4);          // ln2b
   }
+  const size_t extra0 = offs.size();  // per layer: sqkv, s1
+  for (int l = 0; l < D.n_layers; ++l) {
+    take((size_t)3 * d * 4);
+    take((size_t)f * 4);
+  }
   (void)mshape;
   std::vector<uint8_t> host(total, 0);
   auto put_bf16 = [&](int idx, const float* src, int64_t n) {
@@ -332,20 +371,51 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   auto put_f32 = [&](int idx, const float* src, int64_t n) {
     memcpy(host.data() + offs[idx], src, (size_t)n * 4);
   };
+  // LayerNorm folding: src [in, out] row-major -> dst [out, in] holding
+  // bf16(W[i][o] gamma[i]) (one rounding), s[o] = sum_i dst[o][i] (the
+  // rounded values the GEMM uses), b'[o] = b[o] + sum_i W[i][o] beta[i].
+  auto put_folded = [&](int widx, int bidx, size_t sidx, const float* src, const float* bias,
+                        const float* gamma, const float* beta, int64_t in, int64_t outn) {
+    uint16_t* dst = (uint16_t*)(host.data() + offs[widx]);
+    float* bo = (float*)(host.data() + offs[bidx]);
+    float* so = (float*)(host.data() + offs[sidx]);
+    std::vector<double> ssum((size_t)outn, 0.0), csum((size_t)outn, 0.0);
+    for (int64_t i = 0; i < in; ++i)
+      for (int64_t o = 0; o < outn; ++o) {
+        const float wv = src[i * outn + o];
+        const uint16_t q = f32_to_bf16_rne(wv * gamma[i]);
+        dst[o * in + i] = q;
+        uint32_t bits = (uint32_t)q << 16;
+        float qf;
+        memcpy(&qf, &bits, 4);
+        ssum[(size_t)o] += (double)qf;
+        csum[(size_t)o] += (double)wv * (double)beta[i];
+      }
+    for (int64_t o = 0; o < outn; ++o) {
+      so[o] = (float)ssum[(size_t)o];
+      bo[o] = (float)((double)bias[o] + csum[(size_t)o]);
+    }
+  };
   put_bf16(0, host_weights[0], V * d);
   put_bf16(1, host_weights[1], P * d);
   put_f32(2, host_weights[2], d);
   put_f32(3, host_weights[3], d);
   for (int l = 0; l < D.n_layers; ++l) {
     const int b = 4 + 12 * l;
-    put_bf16_t(b + 0, host_weights[b + 0], d, 3 * d);
-    put_f32(b + 1, host_weights[b + 1], 3 * d);
+    if (l == 0) {  // input: the embedding LN's output, already normalised
+      put_bf16_t(b + 0, host_weights[b + 0], d, 3 * d);
+      put_f32(b + 1, host_weights[b + 1], 3 * d);
+    } else {
+      const int pb = 4 + 12 * (l - 1);  // previous layer's LN2
+      put_folded(b + 0, b + 1, extra0 + 2 * l, host_weights[b + 0], host_weights[b + 1],
+                 host_weights[pb + 10], host_weights[pb + 11], d, 3 * d);
+    }
     put_bf16_t(b + 2, host_weights[b + 2], d, d);
     put_f32(b + 3, host_weights[b + 3], d);
     put_f32(b + 4, host_weights[b + 4], d);
     put_f32(b + 5, host_weights[b + 5], d);
-    put_bf16_t(b + 6, host_weights[b + 6], d, f);
-    put_f32(b + 7, host_weights[b + 7], f);
+    put_folded(b + 6, b + 7, extra0 + 2 * l + 1, host_weights[b + 6], host_weights[b + 7],
+               host_weights[b + 4], host_weights[b + 5], d, f);
     put_bf16_t(b + 8, host_weights[b + 8], f, d);
     put_f32(b + 9, host_weights[b + 9], d);
     put_f32(b + 10, host_weights[b + 10], d);
@@ -383,6 +453,8 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
     w.b2 = (float*)(wb + offs[b + 9]);
     w.ln2g = (float*)(wb + offs[b + 10]);
     w.ln2b = (float*)(wb + offs[b + 11]);
+    w.sqkv = l == 0 ? nullptr : (float*)(wb + offs[extra0 + 2 * l]);
+    w.s1 = (float*)(wb + offs[extra0 + 2 * l + 1]);
     e->layers.push_back(w);
   }
 
@@ -404,6 +476,10 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   wtake((size_t)T * 8);            // dst
   wtake((size_t)T * 4);            // attention items
   wtake(256);                      // err
+  wtake((size_t)T * (d / 64) * 8); // SX: at most d/64 partials per row
+  wtake((size_t)T * (d / 64) * 8); // SY
+  wtake((size_t)T * 8);            // RX
+  wtake((size_t)T * 8);            // RY
   err = hipMalloc(&e->wsblock, ws);
   if (err != hipSuccess)
     return cleanup_fail(fail(SURGE_ERR_OUT_OF_MEMORY, "workspace: hipMalloc(%zu) failed: %s", ws,
@@ -419,6 +495,10 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   e->d_dst = (uint64_t*)(w + wo[6]);
   e->d_items = (uint32_t*)(w + wo[7]);
   e->d_err = (int*)(w + wo[8]);
+  e->SX = (float2*)(w + wo[9]);
+  e->SY = (float2*)(w + wo[10]);
+  e->RX = (float2*)(w + wo[11]);
+  e->RY = (float2*)(w + wo[12]);
   err = hipMemset(e->d_err, 0, 256);
   if (err != hipSuccess)
     return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipMemset failed: %s", hipGetErrorString(err)));

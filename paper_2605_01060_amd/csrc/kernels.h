@@ -17,11 +17,48 @@ hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts
                            hipStream_t stream);
 
 // Y[M, N] = epi(X[M, K] W^T + b), W stored [N, K] (out, in), bf16 in/out.
-// epi: 0 = bias, 1 = bias then GELU, 2 = bias then + R[M, N].
 // Requires N % 128 == 0, K % 64 == 0, M >= 1.
-enum LinearEpilogue { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESIDUAL = 2 };
+//   EPI_BIAS          y = acc + b
+//   EPI_BIAS_GELU     y = GELU(acc + b)
+//   EPI_BIAS_RESIDUAL y = acc + b + R
+// LayerNorm folded into its neighbours (post-LN encoder, LN(x) = g (x - mu)
+// rstd + beta per row of x):
+//   EPI_FOLD          X holds raw rows x (K features) whose per-row
+//                     LayerNorm factors are in ex.rows_in; W was built as W diag(g)
+//                     and b as b + W beta, and ex.col_s[n] = sum_k W'[n][k],
+//                     so y = rstd (acc - mu col_s) + b = LN(x) W^T + b;
+//   EPI_FOLD_GELU     the same, then GELU;
+//   EPI_RES_STATS     y = acc + b + R, and the per-row statistics of y go
+//                     to ex.stats_out;
+//   EPI_LNRES_STATS   y = acc + b + LN(R) with R's LayerNorm factors in
+//                     ex.rows_in and LN's g, beta in ex.gamma, ex.beta; the
+//                     statistics of y go to ex.stats_out.
+// Row statistics are partials over linear_stats_width(M, N) consecutive
+// features: float2 (mean, variance) at [p * M + row], p < N / width;
+// launch_ln_rows turns them into the per-row LayerNorm factors
+// float2 (rstd, -mean * rstd) at [row].
+enum LinearEpilogue {
+  EPI_BIAS = 0,
+  EPI_BIAS_GELU = 1,
+  EPI_BIAS_RESIDUAL = 2,
+  EPI_FOLD = 3,
+  EPI_FOLD_GELU = 4,
+  EPI_RES_STATS = 5,
+  EPI_LNRES_STATS = 6,
+};
+struct LinearExtra {
+  const float2* rows_in = nullptr;   // LayerNorm factors of X's rows (FOLD) or R's rows (LNRES)
+  float2* stats_out = nullptr;       // partials of Y's rows (RES_STATS, LNRES_STATS)
+  const float* col_s = nullptr;      // [N] (FOLD)
+  const float* gamma = nullptr;      // [N] (LNRES)
+  const float* beta = nullptr;       // [N] (LNRES)
+};
 hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
-                         uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream);
+                         uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
+                         hipStream_t stream);
+// Features per statistics partial written by launch_linear for an [M, N]
+// output (the width of one wave's slice of a tile).
+int linear_stats_width(int64_t M, int N);
 
 // Packed varlen multi-head self-attention.  qkv bf16 [T, 3 H dh] (Q | K | V
 // column blocks, head h at columns h*dh of each), out bf16 [T, H dh].
@@ -34,6 +71,11 @@ hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* c
 // Work items of a chunk (at most cu[n_texts] of them, every text length in
 // [1, 4096]), longest text first.  Returns the item count.
 int attention_items(const int64_t* cu, int64_t n_texts, uint32_t* items);
+
+// Per-row LayerNorm factors rows[m] = (rstd, -mean * rstd) from `parts`
+// equal-width statistics partials stats[p * M + m] = (mean, variance).
+hipError_t launch_ln_rows(const float2* stats, int parts, int64_t M, float eps, float2* rows,
+                          hipStream_t stream);
 
 // y = LN(x) per row of d (d % 8 == 0, d <= 1024), bf16 in/out.
 hipError_t launch_layernorm(const uint16_t* x, const float* gamma, const float* beta, float eps,

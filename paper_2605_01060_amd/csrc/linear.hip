@@ -97,7 +97,8 @@ template <int BM, int BN, int BK, int NBUF, int WAVES_M, int WAVES_N, int EPI, i
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                         const float* __restrict__ bias, const uint16_t* __restrict__ R,
-                        uint16_t* __restrict__ Y, int M, int N, int K, int tiles_n, int n_tiles) {
+                        uint16_t* __restrict__ Y, int M, int N, int K, int tiles_n, int n_tiles,
+                        LinearExtra ex) {
   constexpr int NWAVES = WAVES_M * WAVES_N;
   constexpr int WM = BM / WAVES_M;  // tokens per wave
   constexpr int WN = BN / WAVES_N;  // features per wave
@@ -129,6 +130,16 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   const int n0 = tn * BN;
   const int wn0 = (wave % WAVES_N) * WN;
   const int wm0 = (wave / WAVES_N) * WM;
+
+  // LayerNorm factors of this lane's rows (fused LayerNorm epilogues),
+  // fetched now so their latency hides behind the main loop.
+  float2 rowf[TM];
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    rowf[j] = make_float2(0.0f, 0.0f);
+    if constexpr (EPI == EPI_FOLD || EPI == EPI_FOLD_GELU || EPI == EPI_LNRES_STATS)
+      rowf[j] = ex.rows_in[min(m0 + wm0 + j * 32 + (lane & 31), M - 1)];
+  }
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -268,13 +279,20 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   // u of row r sits at u ^ (r & 31), so the 32 rows an accumulator register
   // spans fall on distinct banks and a 16-byte pair {2k, 2k+1} stays
   // together (possibly with its halves swapped).
-  //   1. (residual only) every thread copies whole rows of R into the tile
+  //   1. (residual modes) every thread copies whole rows of R into the tile
   //      with 16-byte coalesced loads, all issued before any is used;
-  //   2. each lane adds bias (+ GELU) to its accumulators, adds the residual
-  //      read back from the tile, rounds once to bf16 and writes the tile;
+  //   2. each lane finishes its accumulators (bias or folded LayerNorm,
+  //      GELU, residual read back from the tile), rounds once to bf16 and
+  //      writes the tile; the statistics modes also sum the rounded values
+  //      of each of its rows;
   //   3. every thread stores whole rows of the tile with 16-byte stores.
   {
-        constexpr int U = BN / 4;            // 8-byte units per row
+    constexpr bool FOLD = EPI == EPI_FOLD || EPI == EPI_FOLD_GELU;
+    constexpr bool GELU = EPI == EPI_BIAS_GELU || EPI == EPI_FOLD_GELU;
+    constexpr bool RES = EPI == EPI_BIAS_RESIDUAL || EPI == EPI_RES_STATS || EPI == EPI_LNRES_STATS;
+    constexpr bool LNRES = EPI == EPI_LNRES_STATS;
+    constexpr bool STATS = EPI == EPI_RES_STATS || EPI == EPI_LNRES_STATS;
+    constexpr int U = BN / 4;            // 8-byte units per row
     constexpr int PAIRS = BN / 8;        // 16-byte pairs per row
     constexpr int RPI = NT / PAIRS;      // rows per coalesced iteration
     constexpr int ITER = BM / RPI;
@@ -283,7 +301,18 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
     u32x4* t16 = smem;
     const int cp = threadIdx.x % PAIRS;  // this thread's 16-byte pair in a row
     const int cr = threadIdx.x / PAIRS;
-    if (EPI == EPI_BIAS_RESIDUAL) {
+
+    // Per-row LayerNorm factors (rstd, -mean rstd) of the folded input
+    // (FOLD: X's rows) or of the residual (LNRES: R's rows), loaded before
+    // the main loop.
+    float rs[TM], nm[TM];
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      rs[j] = rowf[j].x;
+      nm[j] = rowf[j].y;
+    }
+
+    if constexpr (RES) {
       u32x4 rv[ITER];
 #pragma unroll
       for (int it = 0; it < ITER; ++it) {
@@ -300,37 +329,87 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
       }
       __syncthreads();
     }
+    float st_s[TM], st_q[TM];
+#pragma unroll
+    for (int j = 0; j < TM; ++j) st_s[j] = st_q[j] = 0.0f;
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int u = (wn0 + i * 32 + 8 * g) / 4 + lhi;
         const float4 bb = *reinterpret_cast<const float4*>(bias + n0 + 4 * u);
+        float4 cs = {0.0f, 0.0f, 0.0f, 0.0f}, gg = cs, be = cs;
+        if constexpr (FOLD) cs = *reinterpret_cast<const float4*>(ex.col_s + n0 + 4 * u);
+        if constexpr (LNRES) {
+          gg = *reinterpret_cast<const float4*>(ex.gamma + n0 + 4 * u);
+          be = *reinterpret_cast<const float4*>(ex.beta + n0 + 4 * u);
+        }
 #pragma unroll
         for (int j = 0; j < TM; ++j) {
           const int r = wm0 + j * 32 + l32;
-          float o0 = acc[i][j][4 * g + 0] + bb.x;
-          float o1 = acc[i][j][4 * g + 1] + bb.y;
-          float o2 = acc[i][j][4 * g + 2] + bb.z;
-          float o3 = acc[i][j][4 * g + 3] + bb.w;
-          if (EPI == EPI_BIAS_GELU) {
+          float o0, o1, o2, o3;
+          if constexpr (FOLD) {
+            o0 = fmaf(rs[j], acc[i][j][4 * g + 0], fmaf(nm[j], cs.x, bb.x));
+            o1 = fmaf(rs[j], acc[i][j][4 * g + 1], fmaf(nm[j], cs.y, bb.y));
+            o2 = fmaf(rs[j], acc[i][j][4 * g + 2], fmaf(nm[j], cs.z, bb.z));
+            o3 = fmaf(rs[j], acc[i][j][4 * g + 3], fmaf(nm[j], cs.w, bb.w));
+          } else {
+            o0 = acc[i][j][4 * g + 0] + bb.x;
+            o1 = acc[i][j][4 * g + 1] + bb.y;
+            o2 = acc[i][j][4 * g + 2] + bb.z;
+            o3 = acc[i][j][4 * g + 3] + bb.w;
+          }
+          if constexpr (GELU) {
             o0 = gelu_erf(o0);
             o1 = gelu_erf(o1);
             o2 = gelu_erf(o2);
             o3 = gelu_erf(o3);
           }
           uint2& cell = t8[r * U + (u ^ (r & 31))];
-          if (EPI == EPI_BIAS_RESIDUAL) {
+          if constexpr (RES) {
             const uint2 rr = cell;
-            o0 += __uint_as_float(rr.x << 16);
-            o1 += __uint_as_float(rr.x & 0xffff0000u);
-            o2 += __uint_as_float(rr.y << 16);
-            o3 += __uint_as_float(rr.y & 0xffff0000u);
+            float r0 = __uint_as_float(rr.x << 16);
+            float r1 = __uint_as_float(rr.x & 0xffff0000u);
+            float r2 = __uint_as_float(rr.y << 16);
+            float r3 = __uint_as_float(rr.y & 0xffff0000u);
+            if constexpr (LNRES) {
+              r0 = fmaf(fmaf(r0, rs[j], nm[j]), gg.x, be.x);
+              r1 = fmaf(fmaf(r1, rs[j], nm[j]), gg.y, be.y);
+              r2 = fmaf(fmaf(r2, rs[j], nm[j]), gg.z, be.z);
+              r3 = fmaf(fmaf(r3, rs[j], nm[j]), gg.w, be.w);
+            }
+            o0 += r0;
+            o1 += r1;
+            o2 += r2;
+            o3 += r3;
           }
           uint2 out;
           out.x = pack_bf16x2(o0, o1);
           out.y = pack_bf16x2(o2, o3);
           cell = out;
+          if constexpr (STATS) {
+            const float v0 = __uint_as_float(out.x << 16), v1 = __uint_as_float(out.x & 0xffff0000u);
+            const float v2 = __uint_as_float(out.y << 16), v3 = __uint_as_float(out.y & 0xffff0000u);
+            st_s[j] += (v0 + v1) + (v2 + v3);
+            st_q[j] = fmaf(v0, v0, fmaf(v1, v1, fmaf(v2, v2, fmaf(v3, v3, st_q[j]))));
+          }
+        }
+      }
+    }
+    if constexpr (STATS) {
+      // This wave's WN features of each of its rows: the lane and its
+      // partner (lane ^ 32) hold complementary halves.  One partial per
+      // (tile, wave column): index tn * WAVES_N + wave column.
+      const int part = tn * WAVES_N + (wave % WAVES_N);
+      constexpr float inv_w = 1.0f / (float)WN;
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const float s1 = st_s[j] + __shfl_xor(st_s[j], 32, 64);
+        const float q1 = st_q[j] + __shfl_xor(st_q[j], 32, 64);
+        const int m = m0 + wm0 + j * 32 + l32;
+        if (lhi == 0 && m < M) {
+          const float mean = s1 * inv_w;
+          ex.stats_out[(size_t)part * M + m] = make_float2(mean, fmaxf(q1 * inv_w - mean * mean, 0.0f));
         }
       }
     }
@@ -353,42 +432,46 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
 
 template <int BM, int BN, int BK, int NBUF, int WAVES_M, int WAVES_N>
 hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
-                        uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream) {
+                        uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
+                        hipStream_t stream) {
   const int tiles_n = N / BN;
   const int64_t tiles_m = (M + BM - 1) / BM;
   const int n_tiles = (int)(tiles_m * tiles_n);
   const dim3 grid((unsigned)n_tiles);
   const dim3 block(WAVES_M * WAVES_N * 64);
+#define SURGE_LAUNCH_EPI(E, O)                                                                \
+  hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, E, O>), grid, block, \
+                     0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles, ex)
   switch (epi) {
-    case EPI_BIAS:
-      hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, EPI_BIAS, ORDER_ROW_GROUPS>),
-                         grid, block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
-      break;
-    case EPI_BIAS_GELU:
-      hipLaunchKernelGGL(
-          (linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, EPI_BIAS_GELU, ORDER_FEATURE_HALVES>), grid,
-          block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
-      break;
-    default:
-      hipLaunchKernelGGL(
-          (linear_bf16_kernel<BM, BN, BK, NBUF, WAVES_M, WAVES_N, EPI_BIAS_RESIDUAL, ORDER_ROW_GROUPS>), grid,
-          block, 0, stream, X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles);
-      break;
+    case EPI_BIAS: SURGE_LAUNCH_EPI(EPI_BIAS, ORDER_ROW_GROUPS); break;
+    case EPI_BIAS_GELU: SURGE_LAUNCH_EPI(EPI_BIAS_GELU, ORDER_FEATURE_HALVES); break;
+    case EPI_BIAS_RESIDUAL: SURGE_LAUNCH_EPI(EPI_BIAS_RESIDUAL, ORDER_ROW_GROUPS); break;
+    case EPI_FOLD: SURGE_LAUNCH_EPI(EPI_FOLD, ORDER_ROW_GROUPS); break;
+    case EPI_FOLD_GELU: SURGE_LAUNCH_EPI(EPI_FOLD_GELU, ORDER_FEATURE_HALVES); break;
+    case EPI_RES_STATS: SURGE_LAUNCH_EPI(EPI_RES_STATS, ORDER_ROW_GROUPS); break;
+    default: SURGE_LAUNCH_EPI(EPI_LNRES_STATS, ORDER_ROW_GROUPS); break;
   }
+#undef SURGE_LAUNCH_EPI
   return hipGetLastError();
 }
 
 }  // namespace
 
+// The tile configuration of an [M, N] output: 256 x 256 tiles (8 waves of
+// 64 tokens x 128 features) where the feature count allows it and there are
+// enough token rows to fill the chip; 128 x 128 tiles (4 waves of 64 x 64)
+// otherwise.
+static bool big_tiles(int64_t M, int N) { return N % 256 == 0 && M >= 8192; }
+
+int linear_stats_width(int64_t M, int N) { return big_tiles(M, N) ? 128 : 64; }
+
 hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
-                         uint16_t* Y, int64_t M, int N, int K, int epi, hipStream_t stream) {
+                         uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
+                         hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  // 256 x 256 tiles (8 waves of 64 tokens x 128 features) where the feature
-  // count allows it and there are enough token rows to fill the chip;
-  // 128 x 128 tiles (4 waves of 64 x 64) otherwise.
-  if (N % 256 == 0 && M >= 8192)
-    return launch_tiles<256, 256, 64, 2, 4, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
-  return launch_tiles<128, 128, 64, 2, 2, 2>(X, W, bias, R, Y, M, N, K, epi, stream);
+  if (big_tiles(M, N))
+    return launch_tiles<256, 256, 64, 2, 4, 2>(X, W, bias, R, Y, M, N, K, epi, ex, stream);
+  return launch_tiles<128, 128, 64, 2, 2, 2>(X, W, bias, R, Y, M, N, K, epi, ex, stream);
 }
 
 }  // namespace surge

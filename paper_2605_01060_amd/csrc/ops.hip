@@ -98,10 +98,57 @@ surge_status surge_op_linear(int64_t M, int32_t N, int32_t K, const uint16_t* d_
       (d_res && !aligned16(d_res)))
     return fail(SURGE_ERR_INVALID_ARGUMENT, "device buffers must be 16-byte aligned");
   hipStream_t s = (hipStream_t)hip_stream;
-  HIP_TRY(launch_linear(d_x, d_w, d_bias, d_res, d_y, M, N, K, epilogue, s));
+  HIP_TRY(launch_linear(d_x, d_w, d_bias, d_res, d_y, M, N, K, epilogue, LinearExtra(), s));
   HIP_TRY(hipStreamSynchronize(s));
   return SURGE_OK;
 }
+
+surge_status surge_op_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                                const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
+                                int32_t epilogue, const float* d_stats_in, int32_t parts_in,
+                                const float* d_col_s, const float* d_gamma, const float* d_beta,
+                                float eps, float* d_stats_out, uint16_t* d_y, void* hip_stream) {
+  clear_error();
+  if (M < 1 || M > (int64_t)INT32_MAX) return fail(SURGE_ERR_INVALID_ARGUMENT, "M=%lld", (long long)M);
+  if (N < 128 || N % 128) return fail(SURGE_ERR_INVALID_ARGUMENT, "N=%d not a multiple of 128", N);
+  if (K < 64 || K % 64) return fail(SURGE_ERR_INVALID_ARGUMENT, "K=%d not a multiple of 64", K);
+  if (epilogue < 0 || epilogue > 6) return fail(SURGE_ERR_INVALID_ARGUMENT, "epilogue=%d", epilogue);
+  const bool fold = epilogue == EPI_FOLD || epilogue == EPI_FOLD_GELU;
+  const bool res = epilogue == EPI_BIAS_RESIDUAL || epilogue >= EPI_RES_STATS;
+  const bool lnres = epilogue == EPI_LNRES_STATS;
+  const bool stats = epilogue >= EPI_RES_STATS;
+  if (!d_x || !d_w || !d_bias || !d_y || (res && !d_res))
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL device pointer");
+  if ((fold || lnres) && (!d_stats_in || parts_in < 1 || parts_in > 1024))
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "stats_in NULL or parts_in=%d outside [1, 1024]",
+                parts_in);
+  if (fold && !d_col_s) return fail(SURGE_ERR_INVALID_ARGUMENT, "col_s is NULL");
+  if (lnres && (!d_gamma || !d_beta)) return fail(SURGE_ERR_INVALID_ARGUMENT, "gamma/beta NULL");
+  if (stats && !d_stats_out) return fail(SURGE_ERR_INVALID_ARGUMENT, "stats_out is NULL");
+  if ((fold || lnres) && !(eps > 0.0f)) return fail(SURGE_ERR_INVALID_ARGUMENT, "eps must be > 0");
+  if (!aligned16(d_x) || !aligned16(d_w) || !aligned16(d_bias) || !aligned16(d_y) ||
+      (d_res && !aligned16(d_res)) || (d_col_s && !aligned16(d_col_s)) ||
+      (d_gamma && !aligned16(d_gamma)) || (d_beta && !aligned16(d_beta)) ||
+      (d_stats_in && ((uintptr_t)d_stats_in & 7u)) || (d_stats_out && ((uintptr_t)d_stats_out & 7u)))
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "device buffers must be aligned (16 B; stats 8 B)");
+  LinearExtra ex;
+  ex.stats_out = (float2*)d_stats_out;
+  ex.col_s = d_col_s;
+  ex.gamma = d_gamma;
+  ex.beta = d_beta;
+  hipStream_t s = (hipStream_t)hip_stream;
+  DeviceCu rows;  // per-row LayerNorm factors, freed on return
+  if (fold || lnres) {
+    HIP_TRY(hipMalloc(&rows.ptr, (size_t)M * 8));
+    HIP_TRY(launch_ln_rows((const float2*)d_stats_in, parts_in, M, eps, (float2*)rows.ptr, s));
+    ex.rows_in = (const float2*)rows.ptr;
+  }
+  HIP_TRY(launch_linear(d_x, d_w, d_bias, d_res, d_y, M, N, K, epilogue, ex, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  return SURGE_OK;
+}
+
+int32_t surge_op_linear_stats_width(int64_t M, int32_t N) { return linear_stats_width(M, N); }
 
 surge_status surge_op_attention(int64_t n_texts, const int64_t* cu, int32_t n_heads, int32_t d_head,
                                 const uint16_t* d_qkv, uint16_t* d_out, void* hip_stream) {

@@ -166,6 +166,33 @@ __global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __
   }
 }
 
+// Per-row LayerNorm factors from equal-width statistics partials (mean,
+// biased variance) at stats[p * M + row]: the row's mean is the average of
+// the partial means and its variance the average partial variance plus the
+// variance of the partial means.  rows[row] = (rstd, -mean * rstd), so that
+// LN(v) = gamma (v rstd - mean rstd) + beta.
+__global__ __launch_bounds__(256) void ln_rows_kernel(const float2* __restrict__ stats, int parts,
+                                                      int64_t M, float eps,
+                                                      float2* __restrict__ rows) {
+  const int64_t m = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (m >= M) return;
+  float sm = 0.0f, sv = 0.0f;
+  for (int p = 0; p < parts; ++p) {
+    const float2 v = stats[(size_t)p * M + m];
+    sm += v.x;
+    sv += v.y;
+  }
+  const float inv_p = 1.0f / (float)parts;
+  const float mu = sm * inv_p;
+  float sd = 0.0f;
+  for (int p = 0; p < parts; ++p) {
+    const float dm = stats[(size_t)p * M + m].x - mu;
+    sd = fmaf(dm, dm, sd);
+  }
+  const float rstd = 1.0f / sqrtf((sv + sd) * inv_p + eps);
+  rows[m] = make_float2(rstd, -mu * rstd);
+}
+
 }  // namespace
 
 hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts,
@@ -175,6 +202,14 @@ hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts
   if (n_texts <= 0) return hipSuccess;
   hipLaunchKernelGGL(embed_ln_kernel, dim3(n_texts), dim3(256), 0, stream, tokens, cu, word, pos,
                      gamma, beta, eps, vocab, d, out, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_rows(const float2* stats, int parts, int64_t M, float eps, float2* rows,
+                          hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL(ln_rows_kernel, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, stream, stats,
+                     parts, M, eps, rows);
   return hipGetLastError();
 }
 

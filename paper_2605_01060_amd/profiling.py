@@ -27,12 +27,14 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 
 # kernel class -> (source file, predicate on the demangled kernel name)
+# (linear epilogues: 0 bias, 1 bias+GELU, 2 residual, 3 folded LN, 4 folded
+# LN + GELU, 5 residual + row statistics, 6 residual LN + row statistics)
 KERNEL_CLASSES = {
-    "qkv": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) == 0),
-    "ffn1": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) == 1),
-    "residual": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) == 2),
+    "qkv": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) in (0, 3)),
+    "ffn1": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) in (1, 4)),
+    "residual": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) in (2, 5, 6)),
     "attn": ("attention.hip", lambda n: "attention_varlen_kernel" in n),
-    "layernorm": ("rows.hip", lambda n: "layernorm_kernel" in n),
+    "layernorm": ("rows.hip", lambda n: "layernorm_kernel" in n or "ln_rows_kernel" in n),
 }
 COPY_KERNEL = "copyBuffer"
 

@@ -83,6 +83,9 @@ _SIGNATURES = {
     "surge_profile_read": ([_P, _P, _I32], _I32),
     "surge_op_embed_ln": ([_I64, _P, _P, _P, _I32, _P, _I32, _P, _P, ctypes.c_float, _I32, _P, _P], _I32),
     "surge_op_linear": ([_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P], _I32),
+    "surge_op_linear_ln": ([_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P, _P, _P,
+                            ctypes.c_float, _P, _P, _P], _I32),
+    "surge_op_linear_stats_width": ([_I64, _I32], _I32),
     "surge_op_attention": ([_I64, _P, _I32, _I32, _P, _P, _P], _I32),
     "surge_op_layernorm": ([_I64, _I32, _P, _P, _P, ctypes.c_float, _P, _P], _I32),
     "surge_op_pool_l2": ([_I64, _P, _I32, _P, _P, _P], _I32),
@@ -291,6 +294,17 @@ def surge_op_embed_ln(cu_seqlens, d_tokens, d_word, vocab, d_pos, max_pos, d_gam
 def surge_op_linear(M, N, K, d_x, d_w, d_bias, d_res, epilogue, d_y, stream=None):
     _check(lib().surge_op_linear(M, N, K, _dev(d_x), _dev(d_w), _dev(d_bias), _dev(d_res),
                                  epilogue, _dev(d_y), _stream(stream)))
+
+
+def surge_op_linear_ln(M, N, K, x, w, bias, res, epilogue, stats_in, parts_in, col_s, gamma,
+                       beta, eps, stats_out, y, stream=None):
+    _check(lib().surge_op_linear_ln(M, N, K, _dev(x), _dev(w), _dev(bias), _dev(res), epilogue,
+                                    _dev(stats_in), parts_in, _dev(col_s), _dev(gamma),
+                                    _dev(beta), eps, _dev(stats_out), _dev(y), _stream(stream)))
+
+
+def surge_op_linear_stats_width(M: int, N: int) -> int:
+    return int(lib().surge_op_linear_stats_width(M, N))
 
 
 def surge_op_attention(cu_seqlens, n_heads, d_head, d_qkv, d_out, stream=None):

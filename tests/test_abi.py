@@ -20,7 +20,7 @@ def declared_functions():
     names = []
     for h in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))):
         text = open(h).read()
-        names += re.findall(r"^\s*(?:surge_status|void|const char\*)\s+(surge_\w+)\s*\(", text,
+        names += re.findall(r"^\s*(?:surge_status|void|int32_t|const char\*)\s+(surge_\w+)\s*\(", text,
                             re.M)
     return names
 

@@ -84,6 +84,84 @@ def test_linear_full_chunk_sampled_rows():
     assert np.all(np.abs(got - ref) <= tol)
 
 
+def _partials(v64, width):
+    """Row statistics partials (mean, biased variance) of consecutive
+    `width`-feature slices, laid out [part, row, 2] as the kernels expect."""
+    M, n = v64.shape
+    parts = v64.reshape(M, n // width, width)
+    st = np.stack([parts.mean(axis=2), parts.var(axis=2)], axis=2)  # [M, P, 2]
+    return np.ascontiguousarray(st.transpose(1, 0, 2))
+
+
+LN_SHAPES = [  # (N, K, M): small tiles with ragged M, and >= 8192 rows for 256 x 256 tiles
+    (2304, 768, 255), (3072, 768, 513), (768, 768, 128), (768, 3072, 200), (1152, 384, 130),
+    (768, 768, 9000), (3072, 768, 8193),
+]
+
+
+@pytest.mark.parametrize("N,K,M", LN_SHAPES)
+@pytest.mark.parametrize("epi", [3, 4, 5, 6])
+def test_linear_layernorm_fused(N, K, M, epi):
+    """The fused forms against the plain definition: LN(x) W^T + b (+GELU)
+    for the folded input, x W^T + b + res or + LN(res) with the output's row
+    statistics, on sampled rows (all rows when M is small)."""
+    torch = torch_cuda()
+    rng = np.random.default_rng(N + 3 * K + 7 * M + 11 * epi)
+    eps = 1e-12
+    x, x64 = _bf16(torch, rng.standard_normal((M, K)) * 1.5 + 0.3)
+    w32 = W.round_to_bf16((rng.standard_normal((N, K)) * 0.05).astype(np.float32))
+    w64 = w32.astype(np.float64)
+    b64 = (rng.standard_normal(N) * 0.1).astype(np.float32).astype(np.float64)
+    res, r64 = _bf16(torch, rng.standard_normal((M, N)) * 2.0 - 0.5)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    fold = epi in (3, 4)
+    width_out = S.surge_op_linear_stats_width(M, N)
+    stats_out = torch.full((N // width_out, M, 2), float("nan"), device="cuda")
+    if fold:
+        g64 = (1.0 + 0.1 * rng.standard_normal(K)).astype(np.float32).astype(np.float64)
+        be64 = (0.1 * rng.standard_normal(K)).astype(np.float32).astype(np.float64)
+        wf = W.round_to_bf16((w32 * g64[None, :].astype(np.float32)).astype(np.float32))
+        col_s = wf.astype(np.float64).sum(axis=1)
+        # the weight the folded GEMM stands for: W' = W_eff diag(gamma) exactly
+        # (bf16(W gamma) differs from W gamma by one rounding; the encoder
+        # tests cover that effect end to end)
+        w64 = wf.astype(np.float64) / g64[None, :]
+        bias = b64 + w64 @ be64
+        width_in = S.surge_op_linear_stats_width(M, K)
+        st_in = _partials(x64, width_in)
+        S.surge_op_linear_ln(M, N, K, x, torch.from_numpy(wf).to(torch.bfloat16).cuda(),
+                             _f32(torch, bias), None, epi, _f32(torch, st_in), K // width_in,
+                             _f32(torch, col_s), None, None, eps, None, y)
+    else:
+        g64 = (1.0 + 0.1 * rng.standard_normal(N)).astype(np.float32).astype(np.float64)
+        be64 = (0.1 * rng.standard_normal(N)).astype(np.float32).astype(np.float64)
+        width_in = S.surge_op_linear_stats_width(M, N)
+        st_in = _partials(r64, width_in)
+        S.surge_op_linear_ln(M, N, K, x, torch.from_numpy(w32).to(torch.bfloat16).cuda(),
+                             _f32(torch, b64), res, epi, _f32(torch, st_in), N // width_in, None,
+                             _f32(torch, g64), _f32(torch, be64), eps, stats_out, y)
+    rows = np.arange(M) if M <= 600 else np.unique(np.concatenate(
+        [np.arange(0, M, 97), [M - 1, M - 2, 255, 256]]))
+    got = _to_np(y)[rows]
+    if fold:
+        ref = E.linear(E.layer_norm(x64[rows], g64, be64, eps), w64.T, b64)
+        if epi == 4:
+            ref = E.gelu(ref)
+    else:
+        r = r64[rows] if epi == 5 else E.layer_norm(r64[rows], g64, be64, eps)
+        ref = E.linear(x64[rows], w64.T, b64) + r
+    err = np.abs(got - ref)
+    tol = BF16_REL * np.abs(ref) + 1e-3 * np.sqrt(np.mean(ref ** 2))
+    assert np.all(err <= tol), (float(err.max()), float((err - tol).max()))
+    if not fold:
+        # statistics of the stored (bf16) rows, per partial
+        st = stats_out.cpu().numpy().astype(np.float64)[:, rows, :]
+        want = _partials(got, width_out)
+        scale = np.mean(got ** 2)
+        assert np.all(np.abs(st[..., 0] - want[..., 0]) <= 1e-5 * np.sqrt(scale) + 1e-6)
+        assert np.all(np.abs(st[..., 1] - want[..., 1]) <= 1e-4 * scale + 1e-6)
+
+
 ATTN_LENGTHS = [1, 2, 3, 4, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 511, 512]
 
 
