@@ -5,6 +5,9 @@
         --kernel-class ffn1 --copy-mib 2048 --command-fetch "..." --command-write "..."
 
 `stats` renders a kernel-trace `*_kernel_stats.csv` as a markdown table.
+`mfma` turns a `--pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES` run into
+the MFMA-busy share of each kernel class (MFMA busy cycles summed over the
+SIMDs / (4 SIMDs x CU busy cycles)).
 `traffic` reads two `--pmc` runs (FETCH_SIZE, then WRITE_SIZE, KiB per
 dispatch), scales each by what the same counter reads for the plain device
 copy of known size that the benchmark runs first (`--copy-calibration-mb`),
@@ -21,7 +24,7 @@ import os
 import re
 import statistics
 import sys
-from typing import Dict, List, Optional
+from typing import Dict, List, Optional, Tuple
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -116,12 +119,35 @@ def load_traffic(kernel_class: str, workload: str) -> Optional[float]:
     return float(rec["bytes_per_launch"])
 
 
+def mfma_busy(csv_path: str) -> Dict[str, Dict[str, float]]:
+    per: Dict[str, Dict[str, float]] = {}
+    rows = list(csv.DictReader(open(csv_path)))
+    by_dispatch: Dict[Tuple[str, str], Dict[str, float]] = {}
+    for r in rows:
+        key = (r.get("Dispatch_Id", r.get("Correlation_Id", "")), r["Kernel_Name"])
+        by_dispatch.setdefault(key, {})[r["Counter_Name"]] = float(r["Counter_Value"])
+    for (_, name), c in by_dispatch.items():
+        if "SQ_VALU_MFMA_BUSY_CYCLES" not in c or "SQ_BUSY_CU_CYCLES" not in c:
+            continue
+        for cls, (_, pred) in KERNEL_CLASSES.items():
+            if pred(name):
+                e = per.setdefault(cls, {"mfma": 0.0, "busy": 0.0, "dispatches": 0})
+                e["mfma"] += c["SQ_VALU_MFMA_BUSY_CYCLES"]
+                e["busy"] += c["SQ_BUSY_CU_CYCLES"]
+                e["dispatches"] += 1
+    return {k: {"mfma_busy_pct": 100.0 * v["mfma"] / (4.0 * v["busy"]) if v["busy"] else 0.0,
+                "dispatches": v["dispatches"]} for k, v in per.items()}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
     a = sub.add_parser("stats")
     a.add_argument("csv")
     a.add_argument("--command", required=True)
+    c = sub.add_parser("mfma")
+    c.add_argument("csv")
+    c.add_argument("--command", required=True)
     b = sub.add_parser("traffic")
     b.add_argument("fetch_csv")
     b.add_argument("write_csv")
@@ -132,6 +158,15 @@ def main(argv=None):
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         sys.stdout.write(stats_markdown(args.csv, args.command))
+    elif args.cmd == "mfma":
+        res = mfma_busy(args.csv)
+        lines = [f"Command: `{args.command}`", "",
+                 "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (4 SIMDs x SQ_BUSY_CU_CYCLES), summed "
+                 "over the dispatches of each kernel class.", "",
+                 "| kernel class | dispatches | MFMA busy % |", "|---|---|---|"]
+        for k in sorted(res):
+            lines.append(f"| {k} | {res[k]['dispatches']} | {res[k]['mfma_busy_pct']:.1f} |")
+        sys.stdout.write("\n".join(lines) + "\n")
     else:
         rec = traffic(args.fetch_csv, args.write_csv, args.kernel_class, args.copy_mib)
         sys.stdout.write(
