@@ -162,6 +162,61 @@ def test_linear_layernorm_fused(N, K, M, epi):
         assert np.all(np.abs(st[..., 1] - want[..., 1]) <= 1e-4 * scale + 1e-6)
 
 
+@pytest.mark.parametrize("epi,N,K", [(4, 3072, 768), (6, 768, 3072), (3, 2304, 768)])
+def test_linear_fused_full_chunk_sampled_rows(epi, N, K):
+    """The fused forms at the size the benchmark launches them (a 262,144-row
+    chunk of bge: FFN1 with LN1 folded in, FFN2 with the residual LN1 and
+    row statistics out, QKV with LN2 folded in), on sampled rows including
+    the last ones."""
+    torch = torch_cuda()
+    M, eps = 262_144, 1e-12
+    g = torch.Generator(device="cuda").manual_seed(epi)
+    x = (torch.randn((M, K), generator=g, device="cuda") * 1.3 + 0.2).to(torch.bfloat16)
+    w = (torch.randn((N, K), generator=g, device="cuda") * 0.05).to(torch.bfloat16)
+    b = torch.randn((N,), generator=g, device="cuda") * 0.1
+    rows = np.unique(np.concatenate([np.arange(0, M, 4099), [M - 1, M - 2, 255, 256]]))
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    rng = np.random.default_rng(epi)
+    if epi in (3, 4):
+        x64 = _to_np(x)
+        width = S.surge_op_linear_stats_width(M, K)
+        st = _partials(x64, width)
+        gam = (1.0 + 0.1 * rng.standard_normal(K)).astype(np.float32).astype(np.float64)
+        bet = (0.1 * rng.standard_normal(K)).astype(np.float32).astype(np.float64)
+        w32 = _to_np(w).astype(np.float32)
+        wf = W.round_to_bf16(w32 * gam[None, :].astype(np.float32))
+        weff = wf.astype(np.float64) / gam[None, :]
+        bias = b.double().cpu().numpy() + weff @ bet
+        S.surge_op_linear_ln(M, N, K, x, torch.from_numpy(wf).to(torch.bfloat16).cuda(),
+                             _f32(torch, bias), None, epi, _f32(torch, st), K // width,
+                             _f32(torch, wf.astype(np.float64).sum(axis=1)), None, None, eps,
+                             None, y)
+        ref = E.linear(E.layer_norm(x64[rows], gam, bet, eps), weff.T, b.double().cpu().numpy())
+        if epi == 4:
+            ref = E.gelu(ref)
+    else:
+        res = (torch.randn((M, N), generator=g, device="cuda") * 1.7 - 0.3).to(torch.bfloat16)
+        r64 = _to_np(res)
+        width = S.surge_op_linear_stats_width(M, N)
+        st = _partials(r64, width)
+        gam = (1.0 + 0.1 * rng.standard_normal(N)).astype(np.float32).astype(np.float64)
+        bet = (0.1 * rng.standard_normal(N)).astype(np.float32).astype(np.float64)
+        stats_out = torch.full((N // width, M, 2), float("nan"), device="cuda")
+        S.surge_op_linear_ln(M, N, K, x, w, b, res, epi, _f32(torch, st), N // width, None,
+                             _f32(torch, gam), _f32(torch, bet), eps, stats_out, y)
+        ref = E.linear(_to_np(x[rows]), _to_np(w).T, b.double().cpu().numpy()) + \
+            E.layer_norm(r64[rows], gam, bet, eps)
+        got_all = _to_np(y[rows])
+        want = _partials(got_all, width)
+        so = stats_out.cpu().numpy().astype(np.float64)[:, rows, :]
+        scale = np.mean(got_all ** 2)
+        assert np.all(np.abs(so[..., 0] - want[..., 0]) <= 1e-5 * np.sqrt(scale) + 1e-6)
+        assert np.all(np.abs(so[..., 1] - want[..., 1]) <= 1e-4 * scale + 1e-6)
+    got = _to_np(y[rows])
+    tol = BF16_REL * np.abs(ref) + 1e-3 * np.sqrt(np.mean(ref ** 2))
+    assert np.all(np.abs(got - ref) <= tol)
+
+
 ATTN_LENGTHS = [1, 2, 3, 4, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 511, 512]
 
 
