@@ -139,12 +139,53 @@ def mfma_busy(csv_path: str) -> Dict[str, Dict[str, float]]:
                 "dispatches": v["dispatches"]} for k, v in per.items()}
 
 
+# bench.py kernel names -> traffic class under profiles/
+BENCH_TRAFFIC = {"qkv": "qkv", "ffn1": "ffn1", "oproj": "residual", "ffn2": "residual",
+                 "attn": "attn", "ln1": "layernorm", "ln2": "layernorm"}
+MFMA_CLASSES = ("qkv", "oproj", "ffn1", "ffn2")
+
+
+def roofline_markdown(bench_json: str, workload: str, command: str,
+                      peak_tflops: float = 2516.6, peak_gbs: float = 8000.0) -> str:
+    """Every kernel class of one benchmark line against its roof: MFMA
+    classes by algorithmic TFLOP/s, the others by algorithmic GB/s, with the
+    measured HBM bytes per launch where profiles/ holds a current figure."""
+    d = json.load(open(bench_json))
+    lines = [f"From `{command}` (one JSON line; per-kernel HIP event times inside the timed "
+             f"region) and the traffic summaries under `profiles/`.", "",
+             f"Value: {d['value']:.0f} texts/s, {d['ms_per_step']:.0f} ms per step, "
+             f"MFMA util {d['mfma_util_pct']:.1f} % of {peak_tflops} TFLOP/s.", "",
+             "| kernel | launches/step | ms/step | achieved | roof | % of roof | "
+             "HBM bytes/launch (measured) | algorithmic bytes/launch |",
+             "|---|---|---|---|---|---|---|---|"]
+    steps = d["steps"]
+    for k, v in d["kernels"].items():
+        per_launch_bytes = None
+        if k in BENCH_TRAFFIC:
+            per_launch_bytes = load_traffic(BENCH_TRAFFIC[k], workload)
+        alg_bytes = v["gbs"] * 1e9 * v["avg_ms"] / 1e3 if "gbs" in v else None
+        if k in MFMA_CLASSES and "tflops" in v:
+            ach, roof, unit = v["tflops"], peak_tflops, "TFLOP/s"
+        else:
+            ach, roof, unit = v.get("gbs", 0.0), peak_gbs, "GB/s"
+        lines.append(
+            f"| {k} | {v['launches'] / steps:.0f} | {v['total_ms_per_step']:.1f} | "
+            f"{ach:.0f} {unit} | {roof:.0f} {unit} | {100 * ach / roof:.1f} | "
+            f"{'%.3g' % per_launch_bytes if per_launch_bytes else '—'} | "
+            f"{'%.3g' % alg_bytes if alg_bytes else '—'} |")
+    return "\n".join(lines) + "\n"
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
     a = sub.add_parser("stats")
     a.add_argument("csv")
     a.add_argument("--command", required=True)
+    r = sub.add_parser("roofline")
+    r.add_argument("bench_json")
+    r.add_argument("--workload", default="bge")
+    r.add_argument("--command", required=True)
     c = sub.add_parser("mfma")
     c.add_argument("csv")
     c.add_argument("--command", required=True)
@@ -158,6 +199,8 @@ def main(argv=None):
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         sys.stdout.write(stats_markdown(args.csv, args.command))
+    elif args.cmd == "roofline":
+        sys.stdout.write(roofline_markdown(args.bench_json, args.workload, args.command))
     elif args.cmd == "mfma":
         res = mfma_busy(args.csv)
         lines = [f"Command: `{args.command}`", "",
