@@ -229,16 +229,14 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
       x2.beta = w.ln1b;
       LAUNCH(SURGE_KERNEL_FFN2, 2.0 * Td * d * f, 2.0 * (Td * f + (double)d * f + 2.0 * Td * d),
              launch_linear(e->H, w.w2, w.b2, e->Y, e->X, T, d, f, EPI_LNRES_STATS, x2, stream));
-      if (l + 1 < D.n_layers)  // the last layer's LN2 is applied below
-        LAUNCH(SURGE_KERNEL_LN2, 0.0, Td * (8.0 * parts + 8.0),
-               launch_ln_rows(e->SX, parts, T, D.ln_eps, e->RX, stream));
+      LAUNCH(SURGE_KERNEL_LN2, 0.0, Td * (8.0 * parts + 8.0),
+             launch_ln_rows(e->SX, parts, T, D.ln_eps, e->RX, stream));
     }
-    // The last layer's LN2, materialised once for pooling.
+    // The last layer's LN2 is applied inside the pooling.
     const LayerWeights& wl = e->layers[D.n_layers - 1];
-    LAUNCH(SURGE_KERNEL_LN2, 0.0, 4.0 * Td * d,
-           launch_layernorm(e->X, wl.ln2g, wl.ln2b, D.ln_eps, e->Y, T, d, stream));
-    LAUNCH(SURGE_KERNEL_POOL, 0.0, 2.0 * Td * d + 4.0 * S * d,
-           launch_pool_l2_scatter(e->Y, e->d_cu, Si, e->d_dst, d, stream));
+    LAUNCH(SURGE_KERNEL_POOL, 0.0, 2.0 * Td * d + 8.0 * Td + 4.0 * S * d,
+           launch_pool_l2_scatter(e->X, e->d_cu, Si, e->d_dst, d, e->RX, wl.ln2g, wl.ln2b,
+                                  stream));
     t0 = t1;
   }
   return SURGE_OK;

@@ -82,8 +82,11 @@ hipError_t launch_layernorm(const uint16_t* x, const float* gamma, const float* 
                             uint16_t* y, int64_t M, int d, hipStream_t stream);
 
 // e_i = mean of text i's rows of x; row i of the output (dst[i], a device
-// pointer to d floats) = e_i / max(||e_i||, 1e-12).
+// pointer to d floats) = e_i / max(||e_i||, 1e-12).  With rows != NULL the
+// rows of x are raw and LayerNorm(gamma, beta) is applied to each first,
+// from its factors rows[t] = (rstd, -mean * rstd).
 hipError_t launch_pool_l2_scatter(const uint16_t* x, const int32_t* cu, int n_texts,
-                                  const uint64_t* dst, int d, hipStream_t stream);
+                                  const uint64_t* dst, int d, const float2* rows,
+                                  const float* gamma, const float* beta, hipStream_t stream);
 
 }  // namespace surge

@@ -206,7 +206,8 @@ surge_status surge_op_pool_l2(int64_t n_texts, const int64_t* cu, int32_t d, con
   HIP_TRY(hipMalloc(&drows.ptr, rows.size() * 8));
   HIP_TRY(hipMemcpy(drows.ptr, rows.data(), rows.size() * 8, hipMemcpyHostToDevice));
   hipStream_t s = (hipStream_t)hip_stream;
-  HIP_TRY(launch_pool_l2_scatter(d_x, dcu.ptr, (int)n_texts, (const uint64_t*)drows.ptr, d, s));
+  HIP_TRY(launch_pool_l2_scatter(d_x, dcu.ptr, (int)n_texts, (const uint64_t*)drows.ptr, d,
+                                 nullptr, nullptr, nullptr, s));
   HIP_TRY(hipStreamSynchronize(s));
   return SURGE_OK;
 }

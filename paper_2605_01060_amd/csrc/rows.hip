@@ -117,10 +117,16 @@ __global__ __launch_bounds__(256) void layernorm_kernel(const uint16_t* __restri
 
 // One block per text: 2 groups of 128 threads split the text's rows, each
 // thread owns one 16-byte column chunk; the norm is a block reduction.
+// With LN, x holds raw rows and row t's LayerNorm is applied on the fly:
+// rows[t] = (rstd, -mean rstd), and the pooled vector is
+// gamma * mean_t(x_t rstd_t - mean_t rstd_t) + beta.
+template <bool LN>
 __global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __restrict__ x,
                                                               const int32_t* __restrict__ cu,
                                                               const uint64_t* __restrict__ dst,
-                                                              int d) {
+                                                              int d, const float2* __restrict__ rows,
+                                                              const float* __restrict__ gamma,
+                                                              const float* __restrict__ beta) {
   __shared__ float part[128 * 8];
   __shared__ float red[4];
   const int t = blockIdx.x;
@@ -134,8 +140,14 @@ __global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __
     for (int p = grp; p < L; p += 2) {
       float f[8];
       unpack8(reinterpret_cast<const uint4*>(x + (size_t)(beg + p) * d)[c], f);
+      if constexpr (LN) {
+        const float2 rf = rows[beg + p];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += f[e];
+        for (int e = 0; e < 8; ++e) acc[e] += fmaf(f[e], rf.x, rf.y);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += f[e];
+      }
     }
   }
   if (grp == 1 && c < nch) {
@@ -149,6 +161,7 @@ __global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       acc[e] = (acc[e] + part[c * 8 + e]) * invL;
+      if constexpr (LN) acc[e] = fmaf(acc[e], gamma[8 * c + e], beta[8 * c + e]);
       sq += acc[e] * acc[e];
     }
   }
@@ -223,9 +236,15 @@ hipError_t launch_layernorm(const uint16_t* x, const float* gamma, const float* 
 }
 
 hipError_t launch_pool_l2_scatter(const uint16_t* x, const int32_t* cu, int n_texts,
-                                  const uint64_t* dst, int d, hipStream_t stream) {
+                                  const uint64_t* dst, int d, const float2* rows,
+                                  const float* gamma, const float* beta, hipStream_t stream) {
   if (n_texts <= 0) return hipSuccess;
-  hipLaunchKernelGGL(pool_l2_scatter_kernel, dim3(n_texts), dim3(256), 0, stream, x, cu, dst, d);
+  if (rows)
+    hipLaunchKernelGGL(pool_l2_scatter_kernel<true>, dim3(n_texts), dim3(256), 0, stream, x, cu,
+                       dst, d, rows, gamma, beta);
+  else
+    hipLaunchKernelGGL(pool_l2_scatter_kernel<false>, dim3(n_texts), dim3(256), 0, stream, x, cu,
+                       dst, d, rows, gamma, beta);
   return hipGetLastError();
 }
 
