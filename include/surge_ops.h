@@ -59,7 +59,7 @@ surge_status surge_op_linear(int64_t M, int32_t N, int32_t K, const uint16_t* d_
  *               and LN's gamma, beta in d_gamma, d_beta [N]; statistics of y
  *               to d_stats_out.
  *   epilogues 0-2 as surge_op_linear.
- * Statistics are partials of W = surge_op_linear_stats_width(M, N)
+ * Statistics are partials of W = surge_op_linear_stats_width(M, N) (64)
  * consecutive features of a row: fp32 pairs (mean, variance) at
  * [(p * M + row) * 2], p < N / W.  d_stats_in holds parts_in partials of
  * equal width per row (the producer's N / W).  Shapes as surge_op_linear;

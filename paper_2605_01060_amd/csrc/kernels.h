@@ -33,8 +33,9 @@ hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts
 //   EPI_LNRES_STATS   y = acc + b + LN(R) with R's LayerNorm factors in
 //                     ex.rows_in and LN's g, beta in ex.gamma, ex.beta; the
 //                     statistics of y go to ex.stats_out.
-// Row statistics are partials over linear_stats_width(M, N) consecutive
-// features: float2 (mean, variance) at [p * M + row], p < N / width;
+// Row statistics are partials over linear_stats_width(M, N) = 64
+// consecutive features in every tile configuration: float2 (mean, variance)
+// at [p * M + row], p < N / 64;
 // launch_ln_rows turns them into the per-row LayerNorm factors
 // float2 (rstd, -mean * rstd) at [row].
 enum LinearEpilogue {

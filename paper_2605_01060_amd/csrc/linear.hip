@@ -42,6 +42,8 @@
 namespace surge {
 namespace {
 
+constexpr int STATS_WIDTH = 64;  // features per row-statistics partial
+
 // Wait until at most `later` stages' copies (CPS instructions each) issued
 // after the one needed next are still in flight.  The vector memory counter
 // retires a wave's loads in issue order.
@@ -329,9 +331,17 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
       }
       __syncthreads();
     }
-    float st_s[TM], st_q[TM];
+    // Statistics partials are 64 features wide in every tile configuration
+    // (two 32-feature accumulator tiles, summed in the same order), so a
+    // row's statistics do not depend on the tile shape of its chunk.
+    constexpr int PW = STATS_WIDTH;
+    constexpr int NPW = WN / PW;  // partials per wave
+    static_assert(WN % PW == 0 && PW % 32 == 0, "statistics partial shape");
+    float st_s[TM][NPW], st_q[TM][NPW];
 #pragma unroll
-    for (int j = 0; j < TM; ++j) st_s[j] = st_q[j] = 0.0f;
+    for (int j = 0; j < TM; ++j)
+#pragma unroll
+      for (int q = 0; q < NPW; ++q) st_s[j][q] = st_q[j][q] = 0.0f;
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
 #pragma unroll
@@ -390,26 +400,30 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
           if constexpr (STATS) {
             const float v0 = __uint_as_float(out.x << 16), v1 = __uint_as_float(out.x & 0xffff0000u);
             const float v2 = __uint_as_float(out.y << 16), v3 = __uint_as_float(out.y & 0xffff0000u);
-            st_s[j] += (v0 + v1) + (v2 + v3);
-            st_q[j] = fmaf(v0, v0, fmaf(v1, v1, fmaf(v2, v2, fmaf(v3, v3, st_q[j]))));
+            const int q = i / (PW / 32);
+            st_s[j][q] += (v0 + v1) + (v2 + v3);
+            st_q[j][q] = fmaf(v0, v0, fmaf(v1, v1, fmaf(v2, v2, fmaf(v3, v3, st_q[j][q]))));
           }
         }
       }
     }
     if constexpr (STATS) {
-      // This wave's WN features of each of its rows: the lane and its
-      // partner (lane ^ 32) hold complementary halves.  One partial per
-      // (tile, wave column): index tn * WAVES_N + wave column.
-      const int part = tn * WAVES_N + (wave % WAVES_N);
-      constexpr float inv_w = 1.0f / (float)WN;
+      // The lane and its partner (lane ^ 32) hold complementary halves of
+      // each PW-feature slice; partial index = first feature / PW.
+      const int part0 = (n0 + wn0) / PW;
+      constexpr float inv_w = 1.0f / (float)PW;
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
-        const float s1 = st_s[j] + __shfl_xor(st_s[j], 32, 64);
-        const float q1 = st_q[j] + __shfl_xor(st_q[j], 32, 64);
         const int m = m0 + wm0 + j * 32 + l32;
-        if (lhi == 0 && m < M) {
-          const float mean = s1 * inv_w;
-          ex.stats_out[(size_t)part * M + m] = make_float2(mean, fmaxf(q1 * inv_w - mean * mean, 0.0f));
+#pragma unroll
+        for (int q = 0; q < NPW; ++q) {
+          const float s1 = st_s[j][q] + __shfl_xor(st_s[j][q], 32, 64);
+          const float q1 = st_q[j][q] + __shfl_xor(st_q[j][q], 32, 64);
+          if (lhi == 0 && m < M) {
+            const float mean = s1 * inv_w;
+            ex.stats_out[(size_t)(part0 + q) * M + m] =
+                make_float2(mean, fmaxf(q1 * inv_w - mean * mean, 0.0f));
+          }
         }
       }
     }
@@ -463,7 +477,7 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
 // otherwise.
 static bool big_tiles(int64_t M, int N) { return N % 256 == 0 && M >= 8192; }
 
-int linear_stats_width(int64_t M, int N) { return big_tiles(M, N) ? 128 : 64; }
+int linear_stats_width(int64_t, int) { return STATS_WIDTH; }
 
 hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                          uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,

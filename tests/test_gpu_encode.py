@@ -104,6 +104,31 @@ def test_tiny_invariant_to_composition_and_chunking():
     assert np.array_equal(a, d)
 
 
+def test_bge_invariant_across_tile_configurations():
+    """bge shapes (d = 768): a chunk of fewer than 8192 tokens runs the
+    128 x 128 GEMM tiles, a larger one the 256 x 256 tiles; the folded
+    LayerNorms' row statistics are built from the same 64-feature partials
+    in both, so every text's embedding is bit-identical either way."""
+    import dataclasses
+    torch = torch_cuda()
+    spec = dataclasses.replace(W.WORKLOADS["bge"], n_texts=400, n_parts=8)
+    wl = W.make_workload(spec)
+    sh = spec.encoder
+    weights = W.make_weights(sh, seed=spec.seed)
+    assert wl.n_tokens > 2 * 8192
+    big = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)  # one chunk, 256-wide tiles
+    a, _ = _encode_all(torch, big, wl, sh.d_model, wl.n_texts, 0)
+    b, nb = _encode_all(torch, big, wl, sh.d_model, 50, 80)  # small SuperBatches
+    big.close()
+    small = S.Encoder(desc_of(sh), weight_list(sh, weights), 4096)  # chunks < 8192 tokens
+    c, _ = _encode_all(torch, small, wl, sh.d_model, wl.n_texts, 0)
+    small.close()
+    assert nb > 4
+    assert not np.isnan(a).any()
+    assert np.array_equal(a, b)
+    assert np.array_equal(a, c)
+
+
 def test_superbatch_entry_point_with_split_partition():
     """surge_encode_superbatch with a hand-made segment table: a SuperBatch
     holding the tail of one partition (row_offset > 0) and the head of the
