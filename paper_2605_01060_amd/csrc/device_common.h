@@ -120,26 +120,28 @@ __device__ __forceinline__ float wave_max(float v) {
 // the outputs it feeds; it needs one reciprocal and no exponential.  With
 // q = 0.5 |z| (1 + c1 |z| + ... + c6 |z|^6)^-16 (c_i = a_i / sqrt(2)^i),
 // both signs of z give GELU(z) = max(z, 0) - q, so no sign fix-up is needed.
+// The factor 0.5 is folded into the polynomial: scaled by k = 2^(1/16), its
+// -16th power carries the 1/2.
 __device__ __forceinline__ float gelu_erf(float z) {
-  constexpr float C1 = 0.0705230784f * 0.70710678118654752f;
-  constexpr float C2 = 0.0422820123f * 0.5f;
-  constexpr float C3 = 0.0092705272f * 0.35355339059327376f;
-  constexpr float C4 = 0.0001520143f * 0.25f;
-  constexpr float C5 = 0.0002765672f * 0.17677669529663688f;
-  constexpr float C6 = 0.0000430638f * 0.125f;
+  constexpr float K = 1.0442737824274138f;  // 2^(1/16)
+  constexpr float C1 = 0.0705230784f * 0.70710678118654752f * K;
+  constexpr float C2 = 0.0422820123f * 0.5f * K;
+  constexpr float C3 = 0.0092705272f * 0.35355339059327376f * K;
+  constexpr float C4 = 0.0001520143f * 0.25f * K;
+  constexpr float C5 = 0.0002765672f * 0.17677669529663688f * K;
+  constexpr float C6 = 0.0000430638f * 0.125f * K;
   const float az = fabsf(z);
   float p = fmaf(C6, az, C5);
   p = fmaf(p, az, C4);
   p = fmaf(p, az, C3);
   p = fmaf(p, az, C2);
   p = fmaf(p, az, C1);
-  p = fmaf(p, az, 1.0f);
+  p = fmaf(p, az, K);
   const float r = __builtin_amdgcn_rcpf(p);
   const float r2 = r * r;
   const float r4 = r2 * r2;
   const float r8 = r4 * r4;
-  const float r16h = (r8 * 0.5f) * r8;
-  return fmaf(-az, r16h, fmaxf(z, 0.0f));
+  return fmaf(-az, r8 * r8, fmaxf(z, 0.0f));
 }
 
 }  // namespace surge

@@ -50,9 +50,6 @@ namespace surge {
 namespace {
 
 constexpr int STATS_WIDTH = 64;  // features per row-statistics partial
-constexpr int BK = 64;           // K per stage
-constexpr int CPR = BK / 8;      // 16-byte chunks per LDS row
-constexpr int RPC = 64 / CPR;    // rows one wave copy instruction fills
 constexpr int EPW = 256;         // 16-byte slots of one wave's epilogue region (4 KB)
 
 // Wait until at most `later` stages' copies (CPS instructions each) issued
@@ -163,7 +160,7 @@ __device__ __forceinline__ uint2 finish4(const float (&a)[4], float4 bb, float4 
   return out;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int EPI, int ORDER>
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int EPI, int ORDER>
 __global__ __launch_bounds__(WAVES_M* WAVES_N * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                         const float* __restrict__ bias, const uint16_t* __restrict__ R,
@@ -174,11 +171,14 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   constexpr int WN = BN / WAVES_N;  // features per wave
   constexpr int TM = WM / 32;       // 32-token accumulator tiles per wave
   constexpr int TN = WN / 32;       // 32-feature accumulator tiles per wave
+  constexpr int CPR = BK / 8;       // 16-byte chunks per LDS row
+  constexpr int RPC = 64 / CPR;     // rows one wave copy instruction fills
   constexpr int XI = BM / (RPC * NWAVES);  // copy instructions per wave per stage, X tile
   constexpr int WI = BN / (RPC * NWAVES);  // ... W tile
   constexpr int SSTAGE = (BM + BN) * CPR;  // 16-byte slots per stage buffer
   static_assert(XI * RPC * NWAVES == BM && WI * RPC * NWAVES == BN, "tile/wave mismatch");
-  static_assert(NWAVES % 2 == 0, "copy slot phase needs an even wave count");
+  static_assert(BK == 32 || BK == 64, "16-byte chunk swizzles exist for 4 and 8 chunks per row");
+  static_assert(CPR == 4 || NWAVES % 2 == 0, "copy slot phase needs an even wave count");
   static_assert(TN % 2 == 0 && STATS_WIDTH == 64, "epilogue passes are 64 features wide");
   // Buffer b holds X rows at smem[b*SSTAGE ..] and W rows after them.
   __shared__ u32x4 smem[2 * SSTAGE];
@@ -483,7 +483,7 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   }
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, int PER_CU>
+template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int PER_CU>
 hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                         uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
                         hipStream_t stream) {
@@ -498,7 +498,7 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
   const dim3 grid((unsigned)std::min<int64_t>(n_tiles, (int64_t)cus * PER_CU));
   const dim3 block(WAVES_M * WAVES_N * 64);
 #define SURGE_LAUNCH_EPI(E, O)                                                                   \
-  hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, WAVES_M, WAVES_N, E, O>), grid, block, 0, stream, \
+  hipLaunchKernelGGL((linear_bf16_kernel<BM, BN, BK, WAVES_M, WAVES_N, E, O>), grid, block, 0, stream, \
                      X, W, bias, R, Y, (int)M, N, K, tiles_n, n_tiles, ex)
   switch (epi) {
     case EPI_BIAS: SURGE_LAUNCH_EPI(EPI_BIAS, ORDER_ROW_GROUPS); break;
@@ -527,8 +527,9 @@ hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias
                          uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
                          hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  if (big_tiles(M, N)) return launch_tiles<256, 256, 4, 2, 1>(X, W, bias, R, Y, M, N, K, epi, ex, stream);
-  return launch_tiles<128, 128, 2, 2, 2>(X, W, bias, R, Y, M, N, K, epi, ex, stream);
+  if (big_tiles(M, N))
+    return launch_tiles<256, 256, 64, 4, 2, 1>(X, W, bias, R, Y, M, N, K, epi, ex, stream);
+  return launch_tiles<128, 128, 64, 2, 2, 2>(X, W, bias, R, Y, M, N, K, epi, ex, stream);
 }
 
 }  // namespace surge
