@@ -97,6 +97,24 @@ __device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
       : "memory", "m0");
 }
 
+// The same copy from a wave-uniform base: lane l fetches the 16 bytes at
+// base + 16 l (a 32-bit lane offset added to a scalar base, computed inside
+// the statement so that no per-lane address has to stay live around it).
+// `lds` must be wave-uniform.
+__device__ __forceinline__ void copy_lanes_to_lds16(const void* base, uint32_t lds) {
+  uint32_t voff;
+  asm volatile(
+      "v_mbcnt_lo_u32_b32 %0, -1, 0\n\t"
+      "v_mbcnt_hi_u32_b32 %0, -1, %0\n\t"
+      "v_lshlrev_b32 %0, 4, %0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      : "=&v"(voff)
+      : "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds))
+      : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_address(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }

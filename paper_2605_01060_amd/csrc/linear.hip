@@ -10,11 +10,20 @@
 //
 // Persistence.  The grid holds as many workgroups as fit on the chip at
 // once; workgroup b computes tiles b, b + G, b + 2G, ... (G = grid size).
-// The copy pipeline runs on across tile boundaries: while a tile's last two
-// stages are on the MFMA units, the next tile's first two stages are being
-// copied, and the epilogue works in a region of its own so those copies
-// need not wait for it.  A tile therefore never starts on an empty
-// pipeline, and no workgroup launch separates two tiles.
+// The copy pipeline runs on across tile boundaries: the next tile's first
+// stage is copied while the current tile's last stage is on the MFMA units,
+// and its second stage as soon as each wave has finished its epilogue.  A
+// tile therefore never starts on an empty pipeline, and no workgroup launch
+// separates two tiles.
+//
+// Epilogue memory.  The buffer released by a tile's last stage is idle
+// until the next tile's second stage is copied into it, so each wave uses
+// the slots its own copies of that stage will fill as its 4 KB epilogue
+// region, and issues those copies when its epilogue is done (no other wave
+// touches the slots, so no barrier is needed).  The tile's per-feature
+// vectors (bias, and the LayerNorm columns of the fused forms) are copied
+// into LDS once per tile at its start, so the epilogue reads them from LDS
+// instead of every lane fetching them again from global memory.
 //
 // Staging.  Stage k+2 is copied straight from global memory into the LDS
 // buffer stage k has just released (global_load_lds_dwordx4, 1 KB per wave
@@ -29,10 +38,10 @@
 // a time over 64 banks.  A copy instruction writes 64 consecutive slots, so
 // each lane fetches the logical chunk that belongs in its slot.
 //
-// Occupancy.  Both configurations run 2 waves per SIMD and fill the LDS:
-// an 8-wave 256 x 256 workgroup takes 128 KB of stage buffers plus 32 KB of
-// epilogue regions (one per CU); a 4-wave 128 x 128 workgroup takes
-// 64 + 16 KB (two per CU).
+// Occupancy.  Both configurations run 2 waves per SIMD: an 8-wave
+// 256 x 256 workgroup takes 128 KB of stage buffers plus at most 6 KB of
+// per-feature vectors (one per CU); a 4-wave 128 x 128 workgroup takes
+// 64 + 3 KB (two per CU).
 //
 // Operand roles.  The MFMA A operand is the weight tile and B the token
 // tile, so the accumulators hold Y^T: each lane owns one token row and four
@@ -50,7 +59,6 @@ namespace surge {
 namespace {
 
 constexpr int STATS_WIDTH = 64;  // features per row-statistics partial
-constexpr int EPW = 256;         // 16-byte slots of one wave's epilogue region (4 KB)
 
 // Wait until at most `later` stages' copies (CPS instructions each) issued
 // after the one needed next are still in flight.  The vector memory counter
@@ -182,10 +190,17 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   static_assert(TN % 2 == 0 && STATS_WIDTH == 64, "epilogue passes are 64 features wide");
   // Buffer b holds X rows at smem[b*SSTAGE ..] and W rows after them.
   __shared__ u32x4 smem[2 * SSTAGE];
-  __shared__ u32x4 sepi[NWAVES * EPW];
+  // Per-feature vectors of the current tile (bias, then col_s or gamma and
+  // beta), double-buffered by the parity of the workgroup's tile count.
+  constexpr bool FOLD_ = EPI == EPI_FOLD || EPI == EPI_FOLD_GELU;
+  constexpr bool LNRES_ = EPI == EPI_LNRES_STATS;
+  constexpr int NV = 1 + (FOLD_ ? 1 : 0) + (LNRES_ ? 2 : 0);
+  static_assert(NV <= NWAVES && BN <= 256, "one vector per wave copy");
+  __shared__ float4 svec[2][NV][BN / 4];
+  static_assert(XI >= 4, "a wave's epilogue region is 4 of its X copy slots");
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: kept in an SGPR
   const int l32 = lane & 31;
   const int lhi = lane >> 5;
   const int wn0 = (wave % WAVES_N) * WN;
@@ -259,12 +274,25 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   static_assert(NM >= NR, "interleave needs at least one MFMA per read");
   bf16x8 fa[2][TN], fb[2][TM];
   int cur_buf = 0;
+  int tpar = 0;
 
   for (;;) {
     int tm, tn;
     tile_coords<ORDER>(t, n_tiles, tiles_n, &tm, &tn);
     const int m0 = tm * BM;
     const int n0 = tn * BN;
+
+    // This tile's per-feature vectors into svec[tpar], wave w copying
+    // vector w (BN floats: one 16-byte chunk per lane).  The main loop's
+    // first stage waits for every copy and meets at a barrier, so the
+    // epilogue finds them in place; the buffer was last read by the
+    // epilogue two tiles back.
+    if (wave < NV && lane < BN / 4) {
+      const float* src = bias;
+      if constexpr (FOLD_) { if (wave == 1) src = ex.col_s; }
+      if constexpr (LNRES_) { if (wave == 1) src = ex.gamma; if (wave == 2) src = ex.beta; }
+      copy_lanes_to_lds16(src + n0, lds_address(&svec[tpar][wave][0]));
+    }
 
     // LayerNorm factors of this lane's rows (fused LayerNorm epilogues),
     // fetched now so their latency hides behind the main loop.
@@ -338,7 +366,8 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this stage's reads are done
       __syncthreads();
-      issue(cur_buf);
+      const bool last_stage = kt == nkt - 1;
+      if (!last_stage) issue(cur_buf);
       cur_buf ^= 1;
       const u32x4* nx = smem + cur_buf * SSTAGE;
       const u32x4* nw = nx + BM * CPR;
@@ -360,7 +389,7 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_group_barrier(0x008, NM - NR, 0);
-      advance();
+      if (!last_stage) advance();
     }
 
     // Epilogue, in passes over this wave's own 4 KB region (no other wave
@@ -386,8 +415,15 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
       constexpr bool STATS = EPI == EPI_RES_STATS || EPI == EPI_LNRES_STATS;
       constexpr int PW = STATS_WIDTH;
       constexpr int NP = TM * (TN / 2);  // passes
-      u32x4* reg16 = sepi + wave * EPW;
-      uint2* reg8 = reinterpret_cast<uint2*>(reg16);
+      // Region row r lives in this wave's X copy slot r/8 of the buffer the
+      // last stage released (8 rows of 128 bytes per 1 KB slot).
+      u32x4* const rbase = smem + (cur_buf ^ 1) * SSTAGE + wave * 64;
+      auto slot16 = [&](int r, int s16) -> u32x4* {
+        return rbase + (r >> 3) * (NWAVES * 64) + (r & 7) * 8 + s16;
+      };
+      auto cell8 = [&](int r, int u) -> uint2* {
+        return reinterpret_cast<uint2*>(slot16(r, 0)) + u;
+      };
       const int cr = lane >> 3;  // row within the 8 rows of one coalesced access
       const int cp = lane & 7;   // 16-byte pair within a row
 
@@ -415,7 +451,7 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
             const int ph = (2 * cp) ^ rsw(r);  // physical unit of logical unit 2cp
             u32x4 v = rv[p][it];
             if (ph & 1) v = u32x4{v[2], v[3], v[0], v[1]};
-            reg16[r * 8 + (ph >> 1)] = v;
+            *slot16(r, ph >> 1) = v;
           }
           asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         }
@@ -426,14 +462,15 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int f = n0 + wn0 + i * 32 + 8 * g + 4 * lhi;  // first of the 4 features
-            const float4 bb = *reinterpret_cast<const float4*>(bias + f);
+            const int fq = (f - n0) >> 2;  // float4 index within the tile
+            const float4 bb = svec[tpar][0][fq];
             float4 cs = {0.0f, 0.0f, 0.0f, 0.0f}, gg = cs, be = cs;
-            if constexpr (FOLD) cs = *reinterpret_cast<const float4*>(ex.col_s + f);
+            if constexpr (FOLD) cs = svec[tpar][1][fq];
             if constexpr (LNRES) {
-              gg = *reinterpret_cast<const float4*>(ex.gamma + f);
-              be = *reinterpret_cast<const float4*>(ex.beta + f);
+              gg = svec[tpar][1][fq];
+              be = svec[tpar][2][fq];
             }
-            uint2& cell = reg8[l32 * 16 + ((8 * ii + 2 * g + lhi) ^ rsw(l32))];
+            uint2& cell = *cell8(l32, (8 * ii + 2 * g + lhi) ^ rsw(l32));
             const float a[4] = {acc[i][j][4 * g + 0], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
                                 acc[i][j][4 * g + 3]};
             const uint2 out = finish4<EPI>(a, bb, cs, gg, be, rs, nm, RES ? cell : uint2{0u, 0u});
@@ -465,7 +502,7 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
         for (int it = 0; it < 4; ++it) {
           const int r = it * 8 + cr;
           const int ph = (2 * cp) ^ rsw(r);
-          ov[it] = reg16[r * 8 + (ph >> 1)];
+          ov[it] = *slot16(r, ph >> 1);
           if (ph & 1) ov[it] = u32x4{ov[it][2], ov[it][3], ov[it][0], ov[it][1]};
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // region free for the next pass
@@ -478,6 +515,11 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
       }
     }
 
+    // The region's reads are done (waited above); this wave's deferred copies
+    // of the next tile's second stage go into the same slots.
+    issue(cur_buf ^ 1);
+    advance();
+    tpar ^= 1;
     t += G;
     if (t >= n_tiles) break;
   }
