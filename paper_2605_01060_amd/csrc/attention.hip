@@ -7,9 +7,18 @@
 //
 // Work decomposition.  A work item is (text, 32-query block); the host
 // lists the items of a chunk longest text first, so the long texts start
-// early and the short ones fill in behind them.  One wave (a workgroup of
-// its own) handles one item for one head: it walks the text's keys in
-// 32-key blocks with an online softmax.
+// early and the short ones fill in behind them.  A unit is one item for one
+// head; a wave (a workgroup of its own) handles UNITS_PER_WAVE units,
+// grid-strided, walking each unit's keys in 32-key blocks with an online
+// softmax.
+//
+// Pipelining.  The wave's key blocks form one sequence across its units:
+// while block j is on the MFMA units, block j+1 is copied into the other
+// buffer, and at a unit's last block that is the next unit's first K/V block
+// together with its Q block.  A unit's output block is staged in the K
+// buffer of its last key block and stored once the next unit's first block
+// has arrived, so every wait is for "everything issued so far" and no wait
+// depends on how many stores were issued.
 //
 // Memory path.  A head's slice of a token row is DH contiguous bf16 (128 B
 // for DH = 64).  Q, K and V blocks move from global memory to LDS with
@@ -37,68 +46,69 @@
 namespace surge {
 namespace {
 
+// Units per wave: enough that most units start on a block copied during
+// the previous unit, few enough that the dispatcher still balances the
+// uneven unit costs across CUs (measured best at 4 on the bge workload).
+constexpr int UNITS_PER_WAVE = 4;
+
 template <int DH>
 __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __restrict__ qkv,
                                                               uint16_t* __restrict__ out,
                                                               const int32_t* __restrict__ cu,
                                                               const uint32_t* __restrict__ items,
-                                                              int n_heads, float scale_log2) {
+                                                              int n_heads, float scale_log2,
+                                                              int n_units) {
   constexpr int KSTEPS = DH / 16;  // MFMA steps over the head dimension for S
   constexpr int DT = DH / 32;      // 32-row tiles of O^T
   constexpr int CPR = DH / 8;      // 16-byte chunks per row
   constexpr int RPC = 64 / CPR;    // rows one wave copy fills
   constexpr int NCP = 32 / RPC;    // copies per 32-row block
   constexpr int BLK = 32 * CPR;    // 16-byte slots per 32-row block
-  // Two K/V buffers.  The Q block passes through the second K buffer before
-  // the first prefetch, and the output block is staged in the first one.
+  // Two K/V buffers (block j of the wave's block sequence in buffer j % 2)
+  // and the Q block of the next unit.  A unit's output block is staged in
+  // the K buffer of its last key block.
   __shared__ u32x4 sK[2][BLK];
   __shared__ u32x4 sV[2][BLK];
-  u32x4* const sQ = sK[1];
-  u32x4* const sO = sK[0];
+  __shared__ u32x4 sQ[BLK];
 
-  const int h = blockIdx.x % n_heads;
-  const uint32_t item = items[blockIdx.x / n_heads];
-  const int t = (int)(item >> 7);
-  const int q0 = (int)(item & 127u) * 32;
   const int lane = threadIdx.x;
   const int col = lane & 31;
   const int half = lane >> 5;
-  const int beg = cu[t];
-  const int L = cu[t + 1] - beg;
   const int D = n_heads * DH;
   const int ld = 3 * D;
-  const uint16_t* Qb = qkv + (size_t)beg * ld + (size_t)h * DH;
-  const uint16_t* Kb = Qb + D;
-  const uint16_t* Vb = Qb + 2 * D;
+  const int crow = lane / CPR;
+  const uint32_t lq = lds_address(sQ);
+  const uint32_t lk = lds_address(sK[0]);
+  const uint32_t lv = lds_address(sV[0]);
+  constexpr uint32_t BUF = BLK * 16;
 
+  // A unit is (work item, head): item = (text << 7 | 32-query block).
+  struct Unit {
+    const uint16_t* base;  // Q row of the text's first token, head h
+    int q0, L, beg, h;
+  };
+  auto unit_at = [&](int u) {
+    Unit r;
+    r.h = u % n_heads;
+    const uint32_t item = items[u / n_heads];
+    const int t = (int)(item >> 7);
+    r.q0 = (int)(item & 127u) * 32;
+    r.beg = cu[t];
+    r.L = cu[t + 1] - r.beg;
+    r.base = qkv + (size_t)r.beg * ld + (size_t)r.h * DH;
+    return r;
+  };
   // Copy j of a 32-row block starting at row r0: lane l fills slot
   // j*64 + l, i.e. row r0 + j*RPC + l/CPR with its swizzled chunk.  Rows past
   // the text are read clamped (their scores are masked, their outputs not
   // stored).
-  const int crow = lane / CPR;
-#define SURGE_COPY_BLOCK(src_, r0_, lds_)                                                   \
-  do {                                                                                      \
-    _Pragma("unroll") for (int j = 0; j < NCP; ++j) {                                       \
-      const int row_ = min((r0_) + j * RPC + crow, L - 1);                                  \
-      copy_to_lds16((src_) + __umul24(row_, ld) + copy_chunk<CPR>(lane, j) * 8,             \
-                    (lds_) + j * 1024);                                                     \
-    }                                                                                       \
-  } while (0)
-
-  const uint32_t lq = lds_address(sK[1]);
-  const uint32_t lk = lds_address(sK[0]);
-  const uint32_t lv = lds_address(sV[0]);
-  constexpr uint32_t BUF = BLK * 16;
-  SURGE_COPY_BLOCK(Qb, q0, lq);
-  SURGE_COPY_BLOCK(Kb, 0, lk);
-  SURGE_COPY_BLOCK(Vb, 0, lv);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-
-  bf16x8 qf[KSTEPS];
+  auto copy_block = [&](const uint16_t* src, int r0, int L, uint32_t lds) {
 #pragma unroll
-  for (int kk = 0; kk < KSTEPS; ++kk)
-    qf[kk] = __builtin_bit_cast(bf16x8, sQ[swz<CPR>(col, kk * 2 + half)]);
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // Q is in registers: sK[1] is free
+    for (int j = 0; j < NCP; ++j) {
+      const int row = min(r0 + j * RPC + crow, L - 1);
+      copy_to_lds16(src + __umul24(row, ld) + copy_chunk<CPR>(lane, j) * 8, lds + j * 1024);
+    }
+  };
 
   // Transposing V reads: lane l supplies the address of 4 features of key
   // 4*half + (l%16)/4 (+ 8 for the second read, + 16c) starting at feature
@@ -108,118 +118,174 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
   const int tr_key = 4 * half + ((lane & 15) >> 2);
   const int tr_feat = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
-  float m_run = -INFINITY;  // running max, log2 units (raw score x scale_log2)
-  float l_run = 0.0f;
-  f32x16 o[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[dt][r] = 0.0f;
+  const int G = gridDim.x;
+  int u = blockIdx.x;  // < n_units: the grid is never larger
+  Unit cur = unit_at(u);
+  copy_block(cur.base, cur.q0, cur.L, lq);
+  copy_block(cur.base + D, 0, cur.L, lk);
+  copy_block(cur.base + 2 * D, 0, cur.L, lv);
 
-  int b = 0;
-  for (int k0 = 0; k0 < L; k0 += 32) {
-    if (k0 > 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // block k0 is in LDS
-    if (k0 + 32 < L) {
-      // The other buffer's reads (previous block) were consumed by MFMAs.
-      SURGE_COPY_BLOCK(Kb, k0 + 32, lk + (b ^ 1) * BUF);
-      SURGE_COPY_BLOCK(Vb, k0 + 32, lv + (b ^ 1) * BUF);
-    }
-    const u32x4* kb = sK[b];
-    const u32x4* vb = sV[b];
+  int b = 0;                      // buffer of the key block being computed
+  bool pending = false;           // a staged output block waits to be stored
+  uint16_t* p_ob = nullptr;       // its destination (first query row, head)
+  int p_rows = 0;                 // and its valid query rows
 
-    // S^T block: rows = keys k0..k0+31 (A operand = K), cols = queries.
-    f32x16 s;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < KSTEPS; ++kk)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          __builtin_bit_cast(bf16x8, kb[swz<CPR>(col, kk * 2 + half)]), qf[kk], s, 0, 0, 0);
+  for (;;) {
+    const int nkb = (cur.L + 31) / 32;
+    const int un = u + G;
+    const bool has_next = un < n_units;
+    Unit nxt = cur;
+    if (has_next) nxt = unit_at(un);
 
-    // Register r holds the score of key k0 + 8*(r/4) + 4*half + r%4; only
-    // the text's last block has keys past its end (uniform branch).
-    if (k0 + 32 > L) {
+    bf16x8 qf[KSTEPS];
+    u32x4 pv[NCP];
+    float m_run = -INFINITY;  // running max, log2 units (raw score x scale_log2)
+    float l_run = 0.0f;
+    f32x16 o[DT];
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (k0 + 8 * (r >> 2) + 4 * half + (r & 3) >= L) s[r] = -INFINITY;
-    }
-    float mloc = s[0];
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc * scale_log2);
-    float psum = 0.0f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -m_new));
-      psum += s[r];
-    }
-    psum += __shfl_xor(psum, 32, 64);
-    if (k0 == 0) {
-      l_run = psum;  // o is still zero: nothing to rescale
-    } else {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run = fmaf(l_run, alpha, psum);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-    }
-    m_run = m_new;
+      for (int r = 0; r < 16; ++r) o[dt][r] = 0.0f;
 
-    // O^T += V^T P^T over two 16-key halves c: slot j of this lane is key
-    // 16c + 8*(j/4) + 4*half + j%4, the same key for the P (B) and V (A)
-    // operands.
-    bf16x8 pb[2];
+    for (int kb = 0; kb < nkb; ++kb) {
+      // Everything this wave issued before is done: the current block (and,
+      // at a unit's first block, its Q), and the stores of the unit before.
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (kb == 0) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+        for (int kk = 0; kk < KSTEPS; ++kk)
+          qf[kk] = __builtin_bit_cast(bf16x8, sQ[swz<CPR>(col, kk * 2 + half)]);
+        if (pending) {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) pb[c][j] = (__bf16)s[8 * c + j];
-    const char* vbytes = reinterpret_cast<const char*>(vb);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      const int feat = dt * 32 + tr_feat;
-#pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        bf16x4 v2[2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const int key = 16 * c + 8 * i + tr_key;
-          const char* pa = vbytes + swz<CPR>(key, feat >> 3) * 16 + (feat & 7) * 2;
-          v2[i] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                                 (__attribute__((address_space(3))) i16x4*)pa));
+          for (int j = 0; j < NCP; ++j) pv[j] = sK[b ^ 1][j * 64 + lane];
         }
-        const bf16x8 va = __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7);
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[c], o[dt], 0, 0, 0);
+        // sQ and the other buffer are read out: they can be refilled.
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
       }
-    }
-    b ^= 1;
-  }
-#undef SURGE_COPY_BLOCK
+      // Prefetch the wave's next block into the other buffer: the next key
+      // block of this unit, or the next unit's Q and first key block.
+      if (kb + 1 < nkb) {
+        copy_block(cur.base + D, (kb + 1) * 32, cur.L, lk + (b ^ 1) * BUF);
+        copy_block(cur.base + 2 * D, (kb + 1) * 32, cur.L, lv + (b ^ 1) * BUF);
+      } else if (has_next) {
+        copy_block(nxt.base, nxt.q0, nxt.L, lq);
+        copy_block(nxt.base + D, 0, nxt.L, lk + (b ^ 1) * BUF);
+        copy_block(nxt.base + 2 * D, 0, nxt.L, lv + (b ^ 1) * BUF);
+      }
+      if (kb == 0 && pending) {
+#pragma unroll
+        for (int j = 0; j < NCP; ++j) {
+          const int row = j * RPC + crow;
+          if (row < p_rows)
+            *reinterpret_cast<u32x4*>(p_ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8) = pv[j];
+        }
+        pending = false;
+      }
+      const int k0 = kb * 32;
+      const u32x4* kbuf = sK[b];
+      const u32x4* vbuf = sV[b];
 
-  // O^T register r of tile dt: head feature dt*32 + 8*(r/4) + 4*half + r%4
-  // of query q0 + col.  Stage the normalised bf16 block in LDS (row =
-  // query), then store whole rows.  All reads of the K/V buffers are done:
-  // their results went into MFMAs.
-  const float inv = 1.0f / l_run;
-  char* obytes = reinterpret_cast<char*>(sO);
+      // S^T block: rows = keys k0..k0+31 (A operand = K), cols = queries.
+      f32x16 s;
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt)
+      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      uint2 w;
-      w.x = pack_bf16x2(o[dt][4 * g + 0] * inv, o[dt][4 * g + 1] * inv);
-      w.y = pack_bf16x2(o[dt][4 * g + 2] * inv, o[dt][4 * g + 3] * inv);
-      *reinterpret_cast<uint2*>(obytes + swz<CPR>(col, dt * 4 + g) * 16 + half * 8) = w;
+      for (int kk = 0; kk < KSTEPS; ++kk)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            __builtin_bit_cast(bf16x8, kbuf[swz<CPR>(col, kk * 2 + half)]), qf[kk], s, 0, 0, 0);
+
+      // Register r holds the score of key k0 + 8*(r/4) + 4*half + r%4; only
+      // the text's last block has keys past its end (uniform branch).
+      if (k0 + 32 > cur.L) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (k0 + 8 * (r >> 2) + 4 * half + (r & 3) >= cur.L) s[r] = -INFINITY;
+      }
+      float mloc = s[0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run, mloc * scale_log2);
+      float psum = 0.0f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -m_new));
+        psum += s[r];
+      }
+      psum += __shfl_xor(psum, 32, 64);
+      if (kb == 0) {
+        l_run = psum;  // o is still zero: nothing to rescale
+      } else {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run = fmaf(l_run, alpha, psum);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      }
+      m_run = m_new;
+
+      // O^T += V^T P^T over two 16-key halves c: slot j of this lane is key
+      // 16c + 8*(j/4) + 4*half + j%4, the same key for the P (B) and V (A)
+      // operands.
+      bf16x8 pb[2];
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) pb[c][j] = (__bf16)s[8 * c + j];
+      const char* vbytes = reinterpret_cast<const char*>(vbuf);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int feat = dt * 32 + tr_feat;
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          bf16x4 v2[2];
+#pragma unroll
+          for (int i = 0; i < 2; ++i) {
+            const int key = 16 * c + 8 * i + tr_key;
+            const char* pa = vbytes + swz<CPR>(key, feat >> 3) * 16 + (feat & 7) * 2;
+            v2[i] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                                   (__attribute__((address_space(3))) i16x4*)pa));
+          }
+          const bf16x8 va = __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7);
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[c], o[dt], 0, 0, 0);
+        }
+      }
+      b ^= 1;
     }
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  uint16_t* ob = out + (size_t)(beg + q0) * D + (size_t)h * DH;
+
+    // O^T register r of tile dt: head feature dt*32 + 8*(r/4) + 4*half + r%4
+    // of query q0 + col.  Stage the normalised bf16 block in the K buffer of
+    // the unit's last key block (row = query; its K reads went into MFMAs).
+    const float inv = 1.0f / l_run;
+    char* obytes = reinterpret_cast<char*>(sK[b ^ 1]);
 #pragma unroll
-  for (int j = 0; j < NCP; ++j) {
-    const int row = j * RPC + crow;
-    const u32x4 v = sO[j * 64 + lane];
-    if (q0 + row < L)
-      *reinterpret_cast<u32x4*>(ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8) = v;
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        uint2 w;
+        w.x = pack_bf16x2(o[dt][4 * g + 0] * inv, o[dt][4 * g + 1] * inv);
+        w.y = pack_bf16x2(o[dt][4 * g + 2] * inv, o[dt][4 * g + 3] * inv);
+        *reinterpret_cast<uint2*>(obytes + swz<CPR>(col, dt * 4 + g) * 16 + half * 8) = w;
+      }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    p_ob = out + (size_t)(cur.beg + cur.q0) * D + (size_t)cur.h * DH;
+    p_rows = cur.L - cur.q0;
+    if (!has_next) {
+      // Last unit of this wave: store now.
+#pragma unroll
+      for (int j = 0; j < NCP; ++j) {
+        const int row = j * RPC + crow;
+        const u32x4 v = sK[b ^ 1][j * 64 + lane];
+        if (row < p_rows)
+          *reinterpret_cast<u32x4*>(p_ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8) = v;
+      }
+      break;
+    }
+    // The next unit's first block stores this one after its data arrived.
+    pending = true;
+    cur = nxt;
+    u = un;
   }
 }
 
@@ -230,13 +296,14 @@ hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* c
                             hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)d_head);
-  const dim3 grid((unsigned)n_items * (unsigned)n_heads);
+  const int n_units = n_items * n_heads;
+  const dim3 grid((unsigned)((n_units + UNITS_PER_WAVE - 1) / UNITS_PER_WAVE));
   if (d_head == 64)
     hipLaunchKernelGGL(attention_varlen_kernel<64>, grid, dim3(64), 0, stream, qkv, out, cu, items,
-                       n_heads, scale_log2);
+                       n_heads, scale_log2, n_units);
   else
     hipLaunchKernelGGL(attention_varlen_kernel<32>, grid, dim3(64), 0, stream, qkv, out, cu, items,
-                       n_heads, scale_log2);
+                       n_heads, scale_log2, n_units);
   return hipGetLastError();
 }
 
