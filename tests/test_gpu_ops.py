@@ -38,6 +38,8 @@ LINEAR_SHAPES = [
     (1152, 384, 130), (384, 384, 257), (1536, 384, 96), (384, 1536, 300),   # MiniLM
     (2304, 768, 255), (768, 768, 128), (3072, 768, 513), (768, 3072, 200),  # bge
     (3072, 1024, 64), (1024, 1024, 100), (4096, 1024, 37), (1024, 4096, 129),  # large
+    # one 64-wide K stage (a tile's first stage is also its last), both tile configurations
+    (128, 64, 300), (256, 64, 8200),
 ]
 
 
@@ -96,6 +98,7 @@ def _partials(v64, width):
 LN_SHAPES = [  # (N, K, M): small tiles with ragged M, and >= 8192 rows for 256 x 256 tiles
     (2304, 768, 255), (3072, 768, 513), (768, 768, 128), (768, 3072, 200), (1152, 384, 130),
     (768, 768, 9000), (3072, 768, 8193),
+    (256, 64, 8200), (128, 64, 77),  # a single K stage per tile
 ]
 
 
