@@ -97,6 +97,18 @@ __device__ __forceinline__ void copy_to_lds16(const void* g, uint32_t lds) {
       : "memory", "m0");
 }
 
+// The same copy from sbase + voff: sbase wave-uniform (scalar registers),
+// voff a 32-bit byte offset per lane.
+__device__ __forceinline__ void copy_to_lds16_at(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
+      : "v"(voff), "s"(sbase), "s"(lds)
+      : "memory", "m0");
+}
+
 // The same copy from a wave-uniform base: lane l fetches the 16 bytes at
 // base + 16 l (a 32-bit lane offset added to a scalar base, computed inside
 // the statement so that no per-lane address has to stay live around it).

@@ -226,25 +226,34 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
   // tile (that work stays off the path between a barrier and the MFMAs).
   int it_tile = blockIdx.x;  // < n_tiles: the grid is never larger than the tile count
   int it_kt = 0;
-  const uint16_t* xg[XI];
-  const uint16_t* wg;
+  // Copy sources: a wave-uniform tile base (scalar registers) plus a 32-bit
+  // byte offset per lane that stays fixed while the tile's stages advance,
+  // so a copy needs no per-lane address arithmetic (the launcher checks that
+  // BM rows of K bf16 fit the 32-bit offset).
+  const uint16_t* xs;  // X row block of the tile
+  const uint16_t* ws;  // W feature block of the tile
+  uint32_t xo[XI], wo[WI];
+#pragma unroll
+  for (int j = 0; j < WI; ++j) wo[j] = (uint32_t)((drow + j * DSTEP) * K + dch * 8) * 2u;
   auto point = [&]() {
     int tm_, tn_;
     tile_coords<ORDER>(it_tile, n_tiles, tiles_n, &tm_, &tn_);
+    xs = X + (size_t)(tm_ * BM) * K;
+    ws = W + (size_t)(tn_ * BN) * K;
 #pragma unroll
     for (int j = 0; j < XI; ++j)  // rows past M: clamped, never stored
-      xg[j] = X + (size_t)min(tm_ * BM + drow + j * DSTEP, M - 1) * K + dch * 8;
-    wg = W + (size_t)(tn_ * BN + drow) * K + dch * 8;
+      xo[j] = (uint32_t)((min(tm_ * BM + drow + j * DSTEP, M - 1) - tm_ * BM) * K + dch * 8) * 2u;
   };
   auto issue = [&](int b) {
     if (it_tile >= n_tiles) return;
     const int ko = it_kt * BK;
     const uint32_t base = lds0 + (uint32_t)b * STAGE_BYTES;
+    const uint16_t* sx = xs + ko;
+    const uint16_t* sw = ws + ko;
 #pragma unroll
-    for (int j = 0; j < XI; ++j) copy_to_lds16(xg[j] + ko, base + j * COPY_BYTES);
+    for (int j = 0; j < XI; ++j) copy_to_lds16_at(sx, xo[j], base + j * COPY_BYTES);
 #pragma unroll
-    for (int j = 0; j < WI; ++j)
-      copy_to_lds16(wg + (size_t)j * DSTEP * K + ko, base + BM * CPR * 16 + j * COPY_BYTES);
+    for (int j = 0; j < WI; ++j) copy_to_lds16_at(sw, wo[j], base + BM * CPR * 16 + j * COPY_BYTES);
   };
   auto advance = [&]() {
     if (++it_kt == nkt) {
@@ -529,6 +538,7 @@ template <int BM, int BN, int BK, int WAVES_M, int WAVES_N, int PER_CU>
 hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                         uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
                         hipStream_t stream) {
+  if ((int64_t)BM * K * 2 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;  // copy offsets
   int dev = 0, cus = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
