@@ -177,7 +177,8 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
         for (int j = 0; j < NCP; ++j) {
           const int row = j * RPC + crow;
           if (row < p_rows)
-            *reinterpret_cast<u32x4*>(p_ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8) = pv[j];
+            __builtin_nontemporal_store(
+                pv[j], reinterpret_cast<u32x4*>(p_ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8));
         }
         pending = false;
       }
@@ -278,7 +279,8 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
         const int row = j * RPC + crow;
         const u32x4 v = sK[b ^ 1][j * 64 + lane];
         if (row < p_rows)
-          *reinterpret_cast<u32x4*>(p_ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8) = v;
+          __builtin_nontemporal_store(
+              v, reinterpret_cast<u32x4*>(p_ob + (size_t)row * D + copy_chunk<CPR>(lane, j) * 8));
       }
       break;
     }

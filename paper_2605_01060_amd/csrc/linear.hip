@@ -519,7 +519,8 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
         for (int it = 0; it < 4; ++it) {
           const int m = m0 + wm0 + j * 32 + it * 8 + cr;
           if (m < M)
-            *reinterpret_cast<u32x4*>(Y + (size_t)m * N + n0 + wn0 + ip * 64 + 8 * cp) = ov[it];
+            __builtin_nontemporal_store(
+                ov[it], reinterpret_cast<u32x4*>(Y + (size_t)m * N + n0 + wn0 + ip * 64 + 8 * cp));
         }
       }
     }
