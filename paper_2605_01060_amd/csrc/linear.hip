@@ -23,7 +23,10 @@
 // touches the slots, so no barrier is needed).  The tile's per-feature
 // vectors (bias, and the LayerNorm columns of the fused forms) are copied
 // into LDS once per tile at its start, so the epilogue reads them from LDS
-// instead of every lane fetching them again from global memory.
+// instead of every lane fetching them again from global memory.  The
+// output rows and the residual rows are touched once per launch, so they
+// are stored and loaded nontemporally, leaving the L2 to the operand tiles
+// that other workgroups read again.
 //
 // Staging.  Stage k+2 is copied straight from global memory into the LDS
 // buffer stage k has just released (global_load_lds_dwordx4, 1 KB per wave
@@ -444,8 +447,8 @@ void linear_bf16_kernel(const uint16_t* __restrict__ X, const uint16_t* __restri
 #pragma unroll
           for (int it = 0; it < 4; ++it) {
             const int m = min(m0 + wm0 + j * 32 + it * 8 + cr, M - 1);
-            rv[p][it] = *reinterpret_cast<const u32x4*>(R + (size_t)m * N + n0 + wn0 + ip * 64 +
-                                                        8 * cp);
+            rv[p][it] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(
+                R + (size_t)m * N + n0 + wn0 + ip * 64 + 8 * cp));
           }
         }
       }
