@@ -259,9 +259,14 @@ surge_status surge_check(surge_encoder* enc, void* hip_stream);
 
 /*
  * Per-kernel timing with HIP events recorded on the encoder's launch stream
- * around each launch.  surge_profile_enable(enc, 1) starts recording (and
- * clears earlier records); surge_profile_read synchronises on the recorded
- * events and returns one entry per kernel class.
+ * around each launch.  surge_profile_enable(enc, 1) starts recording around
+ * every launch (and clears earlier records), surge_profile_enable(enc, 0)
+ * stops; surge_profile_select(enc, mask) records only around the launches
+ * of the kernel classes whose bit (1 << SURGE_KERNEL_*) is set in `mask`
+ * (0 stops; a bit at or above SURGE_KERNEL_COUNT is an invalid argument),
+ * so that timing one class adds no events between the other launches.
+ * surge_profile_read synchronises on the recorded events and returns one
+ * entry per kernel class (zero launches for classes not selected).
  */
 #define SURGE_KERNEL_EMBED 0   /* embedding gather + LayerNorm */
 #define SURGE_KERNEL_QKV 1     /* QKV projection + bias */
@@ -282,6 +287,7 @@ typedef struct surge_kernel_stat {
 } surge_kernel_stat;
 
 surge_status surge_profile_enable(surge_encoder* enc, int32_t on);
+surge_status surge_profile_select(surge_encoder* enc, uint32_t mask);
 surge_status surge_profile_read(surge_encoder* enc, surge_kernel_stat* stats, int32_t n_stats);
 
 #ifdef __cplusplus

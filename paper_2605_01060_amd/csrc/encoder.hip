@@ -75,7 +75,7 @@ struct surge_encoder {
   std::vector<uint64_t> h_dst;
   std::vector<int64_t> h_lcu;
   // profiling
-  bool prof = false;
+  uint32_t prof_kinds = 0;  // bit k set: time launches of kernel class k
   std::vector<hipEvent_t> prof_events;
   int prof_used = 0;
   std::vector<ProfRecord> prof_recs;
@@ -107,9 +107,9 @@ void free_encoder(surge_encoder* e) {
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Profiling: start/stop event pair around one launch.
-surge_status prof_begin(surge_encoder* e, hipStream_t s, int* ev) {
-  if (!e->prof) return SURGE_OK;
+// Profiling: start/stop event pair around one launch of a selected class.
+surge_status prof_begin(surge_encoder* e, hipStream_t s, int kind, int* ev) {
+  if (!((e->prof_kinds >> kind) & 1u)) return SURGE_OK;
   if ((size_t)e->prof_used + 2 > e->prof_events.size()) {
     for (int i = 0; i < 256; ++i) {
       hipEvent_t x;
@@ -125,7 +125,7 @@ surge_status prof_begin(surge_encoder* e, hipStream_t s, int* ev) {
 
 surge_status prof_end(surge_encoder* e, hipStream_t s, int ev, int kind, double flops,
                       double bytes) {
-  if (!e->prof) return SURGE_OK;
+  if (ev < 0) return SURGE_OK;
   HIP_TRY(hipEventRecord(e->prof_events[ev + 1], s));
   e->prof_recs.push_back(ProfRecord{kind, ev, flops, bytes});
   return SURGE_OK;
@@ -134,7 +134,7 @@ surge_status prof_end(surge_encoder* e, hipStream_t s, int ev, int kind, double 
 #define LAUNCH(kind, flops, bytes, call)                             \
   do {                                                               \
     int ev_ = -1;                                                    \
-    surge_status st_ = prof_begin(e, stream, &ev_);                  \
+    surge_status st_ = prof_begin(e, stream, kind, &ev_);            \
     if (st_ != SURGE_OK) return st_;                                 \
     hipError_t le_ = (call);                                         \
     if (le_ != hipSuccess)                                           \
@@ -792,9 +792,16 @@ surge_status surge_check(surge_encoder* enc, void* hip_stream) {
 }
 
 surge_status surge_profile_enable(surge_encoder* enc, int32_t on) {
+  return surge_profile_select(enc, on ? (1u << SURGE_KERNEL_COUNT) - 1u : 0u);
+}
+
+surge_status surge_profile_select(surge_encoder* enc, uint32_t mask) {
   clear_error();
   if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
-  enc->prof = on != 0;
+  if (mask >> SURGE_KERNEL_COUNT)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "kernel class mask 0x%x has bits above class %d",
+                mask, SURGE_KERNEL_COUNT - 1);
+  enc->prof_kinds = mask;
   enc->prof_used = 0;
   enc->prof_recs.clear();
   return SURGE_OK;

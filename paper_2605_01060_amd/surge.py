@@ -80,6 +80,7 @@ _SIGNATURES = {
                                    _P, _I64, _P], _I32),
     "surge_check": ([_P, _P], _I32),
     "surge_profile_enable": ([_P, _I32], _I32),
+    "surge_profile_select": ([_P, ctypes.c_uint32], _I32),
     "surge_profile_read": ([_P, _P, _I32], _I32),
     "surge_op_embed_ln": ([_I64, _P, _P, _P, _I32, _P, _I32, _P, _P, ctypes.c_float, _I32, _P, _P], _I32),
     "surge_op_linear": ([_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P], _I32),
@@ -274,6 +275,14 @@ def surge_profile_enable(handle: int, on: bool):
     _check(lib().surge_profile_enable(handle, 1 if on else 0))
 
 
+def surge_profile_select(handle: int, kinds: Sequence[str]):
+    """Time only the launches of the named kernel classes (empty: none)."""
+    mask = 0
+    for k in kinds:
+        mask |= 1 << KERNEL_NAMES.index(k)
+    _check(lib().surge_profile_select(handle, mask))
+
+
 def surge_profile_read(handle: int) -> Dict[str, Dict[str, float]]:
     stats = (KernelStat * len(KERNEL_NAMES))()
     _check(lib().surge_profile_read(handle, stats, len(KERNEL_NAMES)))
@@ -365,8 +374,11 @@ class Encoder:
     def check(self, stream=None):
         surge_check(self.handle, stream)
 
-    def profile(self, on: bool):
-        surge_profile_enable(self.handle, on)
+    def profile(self, on: bool, kinds: Optional[Sequence[str]] = None):
+        if on and kinds is not None:
+            surge_profile_select(self.handle, kinds)
+        else:
+            surge_profile_enable(self.handle, on)
 
     def profile_read(self):
         return surge_profile_read(self.handle)

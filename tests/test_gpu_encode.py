@@ -235,3 +235,31 @@ def test_full_workload_sampled(name, n_random, n_sb):
     assert np.max(np.abs(norms - 1.0)) < 1e-5
     ref = _oracle_rows(spec, weights, wl, idx)
     assert_parity(got[idx], ref, name)
+
+
+def test_profile_select_times_only_the_selected_class():
+    """Kernel-class selection: with every class timed and with one class
+    selected, the selected class records the same launches and the others
+    none; the outputs are unchanged and a mask beyond the last class is an
+    argument error."""
+    torch = torch_cuda()
+    spec, wl, weights = _setup("tiny")
+    sh = spec.encoder
+    print("[profile_select] tiny workload", flush=True)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    enc.profile(True)
+    ref, _ = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    every = enc.profile_read()
+    enc.profile(True, kinds=["ffn1"])
+    got, _ = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    one = enc.profile_read()
+    enc.profile(False)
+    assert np.array_equal(ref, got)
+    assert every["ffn1"]["launches"] == sh.n_layers
+    assert all(every[k]["launches"] > 0 for k in S.KERNEL_NAMES if k not in ("ln1", "ln2"))
+    for k in S.KERNEL_NAMES:
+        want = every[k]["launches"] if k == "ffn1" else 0
+        assert one[k]["launches"] == want, k
+    assert one["ffn1"]["flops"] == every["ffn1"]["flops"]
+    with pytest.raises(S.SurgeError):
+        S._check(S.lib().surge_profile_select(enc.handle, 1 << len(S.KERNEL_NAMES)))
