@@ -85,6 +85,55 @@ def cpu_baseline(spec, wl, weights, budget_s: float):
             "tokens_per_s": toks / dt}
 
 
+def blas_reference(spec, wl, iters: int = 20):
+    """Vendor GEMM (torch.mm, i.e. hipBLASLt) beside the library's own GEMM
+    with a bias-only epilogue on the encoder's four projection shapes, at
+    the mean SuperBatch token count, on random bf16 data.  Context for the
+    GEMM rooflines only: the encode path never calls a library GEMM."""
+    import torch
+    sh = spec.encoder
+    sbs, _ = S.surge_plan(wl.part_offsets, spec.b_min, spec.n_max)
+    cu = wl.cu_seqlens
+    toks = [int(cu[int(b["text_end"])] - cu[int(b["text_begin"])]) for b in sbs]
+    M = int(round(sum(toks) / len(toks)))
+    d, f = sh.d_model, sh.d_ff
+    shapes = [("qkv", 3 * d, d), ("oproj", d, d), ("ffn1", f, d), ("ffn2", d, f)]
+    g = torch.Generator(device="cuda").manual_seed(0)
+    out = []
+    for name, N, K in shapes:
+        x = torch.randn(M, K, device="cuda", generator=g).to(torch.bfloat16)
+        w = (torch.randn(N, K, device="cuda", generator=g) * 0.03).to(torch.bfloat16)
+        wt = w.t().contiguous()
+        b = torch.zeros(N, device="cuda")
+        y = torch.empty(M, N, device="cuda", dtype=torch.bfloat16)
+        stream = torch.cuda.current_stream()
+
+        def vendor():
+            torch.mm(x, wt, out=y)
+
+        def own():
+            S.surge_op_linear(M, N, K, x, w, b, None, 0, y, stream)
+
+        row = {"gemm": name, "M": M, "N": N, "K": K}
+        for tag, fn in (("hipblaslt_mm", vendor), ("surge_bias_only", own)):
+            for _ in range(5):
+                fn()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(iters):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / iters
+            row[tag + "_ms"] = ms
+            row[tag + "_tflops"] = 2.0 * M * N * K / (ms / 1e3) / 1e12
+        out.append(row)
+        del x, w, wt, b, y
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -100,6 +149,9 @@ def main(argv=None):
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="run one plain device-to-device copy of this many MiB before the "
                          "warm-up (reference for FETCH_SIZE / WRITE_SIZE counter runs)")
+    ap.add_argument("--blas-reference", action="store_true",
+                    help="only time the vendor GEMM beside the library GEMM on the "
+                         "encoder's projection shapes and print them")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -115,6 +167,10 @@ def main(argv=None):
     spec = W.WORKLOADS[args.workload]
     sh = spec.encoder
     wl = W.make_workload(spec)
+    if args.blas_reference:
+        print(json.dumps({"workload": args.workload,
+                          "blas_reference": blas_reference(spec, wl)}), flush=True)
+        return 0
     weights = W.make_weights(sh, seed=spec.seed)
     desc = S.make_desc(sh.n_layers, sh.d_model, sh.n_heads, sh.d_ff, sh.vocab_size,
                        sh.max_positions, sh.ln_eps)
