@@ -151,14 +151,25 @@ def roofline_markdown(bench_json: str, workload: str, command: str,
     classes by algorithmic TFLOP/s, the others by algorithmic GB/s, with the
     measured HBM bytes per launch where profiles/ holds a current figure."""
     d = json.load(open(bench_json))
-    lines = [f"From `{command}` (one JSON line; per-kernel HIP event times inside the timed "
-             f"region) and the traffic summaries under `profiles/`.", "",
+    if d.get("kernels_from"):
+        # per-kernel times from one untimed profiled step; the roofline
+        # kernel timed again inside the timed region
+        src, steps = d["kernels_from"], 1
+    else:
+        src, steps = "HIP events inside the timed region", d["steps"]
+    lines = [f"From `{command}` (one JSON line; per-kernel times: {src}) and the traffic "
+             f"summaries under `profiles/`.", "",
              f"Value: {d['value']:.0f} texts/s, {d['ms_per_step']:.0f} ms per step, "
-             f"MFMA util {d['mfma_util_pct']:.1f} % of {peak_tflops} TFLOP/s.", "",
-             "| kernel | launches/step | ms/step | achieved | roof | % of roof | "
-             "HBM bytes/launch (measured) | algorithmic bytes/launch |",
-             "|---|---|---|---|---|---|---|---|"]
-    steps = d["steps"]
+             f"MFMA util {d['mfma_util_pct']:.1f} % of {peak_tflops} TFLOP/s."]
+    rf = d.get("roofline")
+    if rf:
+        lines.append(f"Roofline kernel `{rf['kernel']}` in the timed region: "
+                     f"{rf['achieved']:.0f} {rf['unit']} of {rf['peak']} "
+                     f"(frac {rf['frac']:.3f}), {rf['avg_launch_ms']:.3f} ms per launch.")
+    lines += ["",
+              "| kernel | launches/step | ms/step | achieved | roof | % of roof | "
+              "HBM bytes/launch (measured) | algorithmic bytes/launch |",
+              "|---|---|---|---|---|---|---|---|"]
     for k, v in d["kernels"].items():
         per_launch_bytes = None
         if k in BENCH_TRAFFIC:
