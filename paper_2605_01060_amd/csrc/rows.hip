@@ -59,7 +59,10 @@ __device__ __forceinline__ void ln_row(float (&v)[MAXC][8], int nch, int lane, i
   }
 }
 
-// One block per text; its four waves take the text's tokens in turn.
+// One block per text; its four waves take the text's tokens in turn.  A
+// wave fetches its next row's token ID and table chunks before it
+// normalises the current row, so one row's gather latency hides behind the
+// previous row's work.
 __global__ __launch_bounds__(256) void embed_ln_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ cu,
     const uint16_t* __restrict__ word, const uint16_t* __restrict__ pos,
@@ -71,7 +74,8 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(
   const int beg = cu[t];
   const int L = cu[t + 1] - beg;
   const int nch = d >> 3;
-  for (int p = wave; p < L; p += 4) {
+  // Table chunks of row p (word row of its checked ID, position row p).
+  auto fetch = [&](int p, uint4 (&w)[MAXC], uint4 (&q)[MAXC]) {
     int id = tokens[beg + p];
     if (id < 0 || id >= vocab) {
       if (lane == 0) atomicOr(err, 1);
@@ -79,18 +83,30 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(
     }
     const uint4* wr = reinterpret_cast<const uint4*>(word + (size_t)id * d);
     const uint4* pr = reinterpret_cast<const uint4*>(pos + (size_t)p * d);
-    float v[MAXC][8];
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
       const int ch = lane + 64 * c;
       if (ch < nch) {
+        w[c] = wr[ch];
+        q[c] = pr[ch];
+      }
+    }
+  };
+  uint4 wn[MAXC], qn[MAXC];
+  if (wave < L) fetch(wave, wn, qn);
+  for (int p = wave; p < L; p += 4) {
+    float v[MAXC][8];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+      if (lane + 64 * c < nch) {
         float a[8], b[8];
-        unpack8(wr[ch], a);
-        unpack8(pr[ch], b);
+        unpack8(wn[c], a);
+        unpack8(qn[c], b);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[c][e] = a[e] + b[e];
       }
     }
+    if (p + 4 < L) fetch(p + 4, wn, qn);
     ln_row(v, nch, lane, d, gamma, beta, eps, out + (size_t)(beg + p) * d);
   }
 }
@@ -183,27 +199,52 @@ __global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __
 // biased variance) at stats[p * M + row]: the row's mean is the average of
 // the partial means and its variance the average partial variance plus the
 // variance of the partial means.  rows[row] = (rstd, -mean * rstd), so that
-// LN(v) = gamma (v rstd - mean rstd) + beta.
+// LN(v) = gamma (v rstd - mean rstd) + beta.  With MAXP > 0 (parts <= MAXP,
+// the encoder's case: d_model / 64 <= 16) every partial is loaded before any
+// is used, so the loads' latencies overlap; MAXP = 0 takes any count.  Both
+// forms sum in the same order.
+template <int MAXP>
 __global__ __launch_bounds__(256) void ln_rows_kernel(const float2* __restrict__ stats, int parts,
                                                       int64_t M, float eps,
                                                       float2* __restrict__ rows) {
   const int64_t m = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (m >= M) return;
-  float sm = 0.0f, sv = 0.0f;
-  for (int p = 0; p < parts; ++p) {
-    const float2 v = stats[(size_t)p * M + m];
-    sm += v.x;
-    sv += v.y;
-  }
+  float sm = 0.0f, sv = 0.0f, sd = 0.0f;
   const float inv_p = 1.0f / (float)parts;
-  const float mu = sm * inv_p;
-  float sd = 0.0f;
-  for (int p = 0; p < parts; ++p) {
-    const float dm = stats[(size_t)p * M + m].x - mu;
-    sd = fmaf(dm, dm, sd);
+  if constexpr (MAXP > 0) {
+    float2 v[MAXP];
+#pragma unroll
+    for (int p = 0; p < MAXP; ++p)
+      if (p < parts) v[p] = stats[(size_t)p * M + m];
+#pragma unroll
+    for (int p = 0; p < MAXP; ++p)
+      if (p < parts) {
+        sm += v[p].x;
+        sv += v[p].y;
+      }
+    const float mu = sm * inv_p;
+#pragma unroll
+    for (int p = 0; p < MAXP; ++p)
+      if (p < parts) {
+        const float dm = v[p].x - mu;
+        sd = fmaf(dm, dm, sd);
+      }
+    const float rstd = 1.0f / sqrtf((sv + sd) * inv_p + eps);
+    rows[m] = make_float2(rstd, -mu * rstd);
+  } else {
+    for (int p = 0; p < parts; ++p) {
+      const float2 v = stats[(size_t)p * M + m];
+      sm += v.x;
+      sv += v.y;
+    }
+    const float mu = sm * inv_p;
+    for (int p = 0; p < parts; ++p) {
+      const float dm = stats[(size_t)p * M + m].x - mu;
+      sd = fmaf(dm, dm, sd);
+    }
+    const float rstd = 1.0f / sqrtf((sv + sd) * inv_p + eps);
+    rows[m] = make_float2(rstd, -mu * rstd);
   }
-  const float rstd = 1.0f / sqrtf((sv + sd) * inv_p + eps);
-  rows[m] = make_float2(rstd, -mu * rstd);
 }
 
 }  // namespace
@@ -221,8 +262,12 @@ hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts
 hipError_t launch_ln_rows(const float2* stats, int parts, int64_t M, float eps, float2* rows,
                           hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL(ln_rows_kernel, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, stream, stats,
-                     parts, M, eps, rows);
+  if (parts < 1) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)((M + 255) / 256));
+  if (parts <= 16)
+    hipLaunchKernelGGL(ln_rows_kernel<16>, grid, dim3(256), 0, stream, stats, parts, M, eps, rows);
+  else
+    hipLaunchKernelGGL(ln_rows_kernel<0>, grid, dim3(256), 0, stream, stats, parts, M, eps, rows);
   return hipGetLastError();
 }
 
