@@ -226,8 +226,13 @@ typedef struct surge_stream_stats {
  * `copy_stream`, double-buffered, so the download of SuperBatch j and the
  * upload of j+1 overlap the encode of j+1 on `compute_stream` (Sec. 3.3,
  * Alg. 2 on the PCIe side of the GPU).  With overlap = 0 everything runs on
- * `compute_stream` in order (the synchronous baseline).  Returns after both
- * streams have finished.
+ * `compute_stream` in order (the synchronous baseline).  With overlap = 2
+ * (zero copy) the tokens are uploaded in order on `compute_stream` and the
+ * pooling kernel writes every embedding straight into h_out through its
+ * device mapping, so no download runs at all; h_out must then be pinned
+ * host memory mapped for the device (hipHostMalloc) over all n_texts rows,
+ * else SURGE_ERR_INVALID_ARGUMENT before anything runs, and the download
+ * times read 0.  Returns after both streams have finished.
  *
  * h_token_ids: host int32 [h_cu_seqlens[n_texts]], texts back to back.
  * h_cu_seqlens: host int64 [n_texts+1], global.  h_part_offsets: host int64
@@ -236,8 +241,8 @@ typedef struct surge_stream_stats {
  *   partition p's E_p is rows part_offsets[p] .. part_offsets[p+1]-1.
  *   h_token_ids and h_out should be pinned (hipHostMalloc); pageable memory
  *   works but its copies do not overlap.
- * copy_stream: a second stream (ignored when overlap = 0); both streams may
- *   be NULL only when overlap = 0.
+ * copy_stream: a second stream (used only when overlap = 1); both streams
+ *   may be NULL when overlap is 0 or 2.
  * h_sb_times: optional [sb_times_cap * 3] doubles; receives (upload, encode,
  *   download) ms of SuperBatch j at 3j .. 3j+2 for j < sb_times_cap.
  * stats: optional, receives the timing summary.

@@ -611,8 +611,8 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   if (!h_part_offsets || !h_cu_seqlens) return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL host array");
   if (n_parts < 0 || h_part_offsets[n_parts] != n_texts)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts] != n_texts");
-  if (overlap != 0 && overlap != 1) return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap=%d", overlap);
-  if (overlap && compute_stream == copy_stream)
+  if (overlap < 0 || overlap > 2) return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap=%d", overlap);
+  if (overlap == 1 && compute_stream == copy_stream)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap needs two different streams");
   if (h_sb_times == nullptr && sb_times_cap != 0)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "sb_times_cap > 0 with NULL h_sb_times");
@@ -639,7 +639,26 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   HIP_TRY(hipSetDevice(enc->device));
   surge_encoder* e = enc;
   hipStream_t cs = (hipStream_t)compute_stream;
-  hipStream_t xs = overlap ? (hipStream_t)copy_stream : cs;
+  hipStream_t xs = overlap == 1 ? (hipStream_t)copy_stream : cs;
+  const bool zero_copy = overlap == 2;
+  // Zero copy: the pooling kernel writes the embeddings through the device
+  // mapping of h_out, which must be pinned host memory mapped for this
+  // device over its whole extent (checked here, before anything runs).
+  float* d_out_mapped = nullptr;
+  if (zero_copy) {
+    const size_t bytes = (size_t)n_texts * (size_t)d * sizeof(float);
+    hipPointerAttribute_t a0, a1;
+    const bool ok0 = hipPointerGetAttributes(&a0, h_out) == hipSuccess;
+    const bool ok1 = ok0 && hipPointerGetAttributes(&a1, (const char*)h_out + bytes - 1) == hipSuccess;
+    (void)hipGetLastError();  // a failed query leaves no sticky error behind
+    if (!ok1 || a0.type != hipMemoryTypeHost || a1.type != hipMemoryTypeHost ||
+        a0.devicePointer == nullptr ||
+        (const char*)a1.devicePointer != (const char*)a0.devicePointer + bytes - 1)
+      return fail(SURGE_ERR_INVALID_ARGUMENT,
+                  "overlap=2 needs h_out in pinned host memory mapped for the device "
+                  "(hipHostMalloc) over all %lld rows", (long long)n_texts);
+    d_out_mapped = (float*)a0.devicePointer;
+  }
 
   int64_t max_tok = 0, max_txt = 0;
   for (const PlanSB& sb : plan.sbs) {
@@ -667,7 +686,7 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   r.s2 = xs;
   for (int i = 0; i < 2; ++i) {
     HIP_TRY(hipMalloc(&r.tok[i], (size_t)std::max<int64_t>(max_tok, 1) * 4));
-    HIP_TRY(hipMalloc(&r.out[i], (size_t)max_txt * d * 4));
+    if (!zero_copy) HIP_TRY(hipMalloc(&r.out[i], (size_t)max_txt * d * 4));
   }
   // Six events per SuperBatch: upload, encode and download start / end.
   r.ev.resize((size_t)ns * 6, nullptr);
@@ -688,8 +707,9 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
     const PlanSB& sb = plan.sbs[(size_t)j];
     const int64_t S = sb.text_end - sb.text_begin;
     HIP_TRY(hipEventRecord(EV(j, D2H0), xs));
-    HIP_TRY(hipMemcpyAsync(h_out + sb.text_begin * d, r.out[j & 1], (size_t)S * d * 4,
-                           hipMemcpyDeviceToHost, xs));
+    if (!zero_copy)  // (zero copy: the rows are already in h_out)
+      HIP_TRY(hipMemcpyAsync(h_out + sb.text_begin * d, r.out[j & 1], (size_t)S * d * 4,
+                             hipMemcpyDeviceToHost, xs));
     HIP_TRY(hipEventRecord(EV(j, D2H1), xs));
     return SURGE_OK;
   };
@@ -699,14 +719,17 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   for (int64_t j = 0; j < ns; ++j) {
     const PlanSB& sb = plan.sbs[(size_t)j];
     const int64_t S = sb.text_end - sb.text_begin;
-    if (overlap) {
+    if (overlap == 1) {
       HIP_TRY(hipStreamWaitEvent(cs, EV(j, H2D1), 0));
       if (j >= 2) HIP_TRY(hipStreamWaitEvent(cs, EV(j - 2, D2H1), 0));  // staging j&1 is free
     }
-    // Rows of this SuperBatch's texts in the embedding staging buffer.
+    // Rows of this SuperBatch's texts: in the embedding staging buffer, or
+    // (zero copy) in the device mapping of h_out.
     e->h_dst.resize((size_t)S);
     for (int64_t i = 0; i < S; ++i)
-      e->h_dst[(size_t)i] = (uint64_t)(uintptr_t)(r.out[j & 1] + i * d);
+      e->h_dst[(size_t)i] =
+          zero_copy ? (uint64_t)(uintptr_t)(d_out_mapped + (sb.text_begin + i) * d)
+                    : (uint64_t)(uintptr_t)(r.out[j & 1] + i * d);
     lcu.resize((size_t)S + 1);
     const int64_t base = h_cu_seqlens[sb.text_begin];
     for (int64_t i = 0; i <= S; ++i) lcu[(size_t)i] = h_cu_seqlens[sb.text_begin + i] - base;
@@ -714,7 +737,7 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
     st = encode_chunks(e, S, r.tok[j & 1], lcu.data(), cs);
     if (st != SURGE_OK) return st;
     HIP_TRY(hipEventRecord(EV(j, ENC1), cs));
-    if (overlap) {
+    if (overlap == 1) {
       if (j + 1 < ns) {
         if (j >= 1) HIP_TRY(hipStreamWaitEvent(xs, EV(j - 1, ENC1), 0));  // tokens j+1 & 1 free
         st = upload(j + 1);
@@ -744,7 +767,7 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   for (int64_t j = 0; j < ns; ++j) {
     const double u = span(EV(j, H2D0), EV(j, H2D1));
     const double c = span(EV(j, ENC0), EV(j, ENC1));
-    const double w = span(EV(j, D2H0), EV(j, D2H1));
+    const double w = zero_copy ? 0.0 : span(EV(j, D2H0), EV(j, D2H1));
     h2d_ms += u;
     enc_ms += c;
     d2h_ms += w;

@@ -57,7 +57,7 @@ def _streamed(torch, enc, wl, d, b_min, n_max, overlap):
     return h_out.numpy().copy(), st, times
 
 
-@pytest.mark.parametrize("overlap", [1, 0])
+@pytest.mark.parametrize("overlap", [1, 0, 2])
 def test_streamed_matches_encode_all(overlap):
     torch = torch_cuda()
     spec, wl, weights = _workload("minilm", n_texts=12000)
@@ -73,7 +73,11 @@ def test_streamed_matches_encode_all(overlap):
     np.testing.assert_array_equal(got, ref)
     assert st["total_ms"] > 0 and 0 < st["ttfo_ms"] <= st["total_ms"]
     assert 0.0 <= st["rho"] <= 1.0 and 0.0 <= st["rho_measured"] <= 1.0
-    assert np.all(times > 0)
+    assert np.all(times[:, :2] > 0)
+    if overlap == 2:  # zero copy: no download step
+        assert np.all(times[:, 2] == 0) and st["d2h_ms"] == 0
+    else:
+        assert np.all(times[:, 2] > 0)
     assert st["enc_ms"] == pytest.approx(times[:, 1].sum(), rel=1e-6)
     if overlap == 0:
         # one stream: the phases add up
@@ -117,6 +121,18 @@ def test_streamed_invalid_arguments():
     with pytest.raises(S.SurgeError):
         enc.encode_all_streamed(wl.n_texts, h_tok, wl.cu_seqlens, bad, spec.b_min, spec.n_max,
                                 h_out, overlap=0, compute_stream=cs)
+    # zero copy needs pinned (device-mapped) output memory: pageable memory
+    # is refused before anything runs
+    pageable = np.zeros((wl.n_texts, sh.d_model), np.float32)
+    with pytest.raises(S.SurgeError) as ei:
+        enc.encode_all_streamed(wl.n_texts, h_tok, wl.cu_seqlens, wl.part_offsets, spec.b_min,
+                                spec.n_max, pageable, overlap=2, compute_stream=cs)
+    assert ei.value.status == S.SURGE_ERR_INVALID_ARGUMENT
+    assert np.all(pageable == 0)
+    with pytest.raises(S.SurgeError) as ei:  # no such mode
+        enc.encode_all_streamed(wl.n_texts, h_tok, wl.cu_seqlens, wl.part_offsets, spec.b_min,
+                                spec.n_max, h_out, overlap=3, compute_stream=cs)
+    assert ei.value.status == S.SURGE_ERR_INVALID_ARGUMENT
     # an out-of-vocabulary token is reported after the run
     tok = wl.tokens.copy()
     tok[5] = sh.vocab_size + 7
