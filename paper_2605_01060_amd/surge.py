@@ -251,9 +251,10 @@ def surge_encode_all_streamed(handle: int, n_texts: int, h_token_ids, cu_seqlens
                               compute_stream=None, copy_stream=None,
                               sb_times: Optional[np.ndarray] = None) -> Dict[str, float]:
     """h_token_ids / h_out: host buffers (pinned torch CPU tensors or NumPy
-    arrays; pass pinned memory for overlapping copies).  Returns the timing
-    summary; per-SuperBatch (upload, encode, download) ms go to sb_times
-    [cap, 3] float64 if given."""
+    arrays; pass pinned memory for overlapping copies).  overlap: 0 in order
+    on compute_stream, 1 copies on copy_stream, 2 zero copy (h_out must be
+    pinned).  Returns the timing summary; per-SuperBatch (upload, encode,
+    download) ms go to sb_times [cap, 3] float64 if given."""
     cu, pcu = _host(cu_seqlens, np.int64)
     offs, poff = _host(part_offsets, np.int64)
     st = StreamStats()
