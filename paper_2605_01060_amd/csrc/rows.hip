@@ -153,6 +153,9 @@ __global__ __launch_bounds__(256) void pool_l2_scatter_kernel(const uint16_t* __
   const int nch = d >> 3;
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   if (c < nch) {
+    // Unrolled so that several rows' loads are in flight at once (the sum
+    // keeps its row order).
+#pragma unroll 4
     for (int p = grp; p < L; p += 2) {
       float f[8];
       unpack8(reinterpret_cast<const uint4*>(x + (size_t)(beg + p) * d)[c], f);
