@@ -1,0 +1,120 @@
+"""Host logic of the measurement helpers (no GPU): kernel classification of
+rocprofv3 names, the copy-calibrated traffic arithmetic, the source-hash
+gate on stored traffic figures, the MFMA-busy share, the roofline summary,
+and bench.py's refusal of more than one GPU."""
+import csv
+import json
+import os
+
+import pytest
+
+import bench
+from paper_2605_01060_amd import profiling as P
+
+LIN = "void surge::(anonymous namespace)::linear_bf16_kernel<256, 256, 64, 4, 2, {epi}, {order}>(x)"
+ATTN = "void surge::(anonymous namespace)::attention_varlen_kernel<64>(x)"
+COPY = "__amd_rocclr_copyBuffer"
+
+
+def _classes(name):
+    return [c for c, (_, pred) in P.KERNEL_CLASSES.items() if pred(name)]
+
+
+def test_kernel_classification():
+    assert P._epi(LIN.format(epi=4, order=1)) == 4
+    assert P._epi(ATTN) == -1
+    assert _classes(LIN.format(epi=0, order=0)) == ["qkv"]
+    assert _classes(LIN.format(epi=3, order=0)) == ["qkv"]
+    assert _classes(LIN.format(epi=4, order=1)) == ["ffn1"]
+    for epi in (2, 5, 6):
+        assert _classes(LIN.format(epi=epi, order=0)) == ["residual"]
+    assert _classes(ATTN) == ["attn"]
+    assert _classes("void surge::(anonymous namespace)::ln_rows_kernel<16>(x)") == ["layernorm"]
+    assert _classes(COPY) == []
+
+
+def _counter_csv(path, counter, rows):
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for i, (name, value) in enumerate(rows):
+            w.writerow([i, name, counter, value])
+
+
+def test_traffic_scales_by_the_calibration_copy(tmp_path):
+    copy_mib = 2048
+    # the copy reads half of its bytes through FETCH_SIZE (scale 2) and all of
+    # them through WRITE_SIZE (scale 1); smaller copies are not the calibration
+    fetch = tmp_path / "fetch.csv"
+    write = tmp_path / "write.csv"
+    ffn1 = LIN.format(epi=4, order=1)
+    _counter_csv(fetch, "FETCH_SIZE", [(COPY, 1024.0), (COPY, copy_mib * 512.0),
+                                       (ffn1, 1000.0), (ffn1, 3000.0), (ATTN, 7.0)])
+    _counter_csv(write, "WRITE_SIZE", [(COPY, copy_mib * 1024.0), (ffn1, 500.0),
+                                       (ffn1, 700.0)])
+    rec = P.traffic(str(fetch), str(write), "ffn1", copy_mib)
+    assert rec["fetch_scale"] == pytest.approx(2.0)
+    assert rec["write_scale"] == pytest.approx(1.0)
+    assert rec["fetch_dispatches"] == 2 and rec["write_dispatches"] == 2
+    assert rec["fetch_bytes_per_launch"] == pytest.approx(2000.0 * 1024 * 2.0)
+    assert rec["write_bytes_per_launch"] == pytest.approx(600.0 * 1024 * 1.0)
+    assert rec["bytes_per_launch"] == pytest.approx(2000.0 * 2048 + 600.0 * 1024)
+    assert rec["source_sha256"] == P.source_hash("ffn1")
+    _counter_csv(fetch, "FETCH_SIZE", [(ffn1, 1.0)])
+    with pytest.raises(SystemExit):  # no calibration copy in the run
+        P.traffic(str(fetch), str(write), "ffn1", copy_mib)
+
+
+def _traffic_md(root, cls, sha, value):
+    os.makedirs(root / "profiles", exist_ok=True)
+    rec = {"kernel_class": cls, "source_sha256": sha, "bytes_per_launch": value}
+    (root / "profiles" / f"traffic_{cls}_bge.md").write_text(
+        "header\n\n```json\n" + json.dumps(rec) + "\n```\n")
+
+
+def test_stored_traffic_is_dropped_once_the_source_changes(tmp_path, monkeypatch):
+    monkeypatch.setattr(P, "ROOT", str(tmp_path))
+    assert P.load_traffic("attn", "bge") is None  # absent
+    _traffic_md(tmp_path, "attn", P.source_hash("attn"), 1.5e9)
+    assert P.load_traffic("attn", "bge") == pytest.approx(1.5e9)
+    _traffic_md(tmp_path, "attn", "0" * 64, 1.5e9)  # taken on another source
+    assert P.load_traffic("attn", "bge") is None
+
+
+def test_mfma_busy_share(tmp_path):
+    path = tmp_path / "mfma.csv"
+    ffn1 = LIN.format(epi=4, order=1)
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for d, (mfma, busy) in enumerate([(400.0, 200.0), (200.0, 100.0)]):
+            w.writerow([d, ffn1, "SQ_VALU_MFMA_BUSY_CYCLES", mfma])
+            w.writerow([d, ffn1, "SQ_BUSY_CU_CYCLES", busy])
+        w.writerow([9, ATTN, "SQ_VALU_MFMA_BUSY_CYCLES", 1.0])  # incomplete pair
+    res = P.mfma_busy(str(path))
+    assert res["ffn1"]["dispatches"] == 2
+    assert res["ffn1"]["mfma_busy_pct"] == pytest.approx(100.0 * 600.0 / (4 * 300.0))
+    assert "attn" not in res
+
+
+def test_roofline_summary_reads_one_profiled_step(tmp_path, monkeypatch):
+    monkeypatch.setattr(P, "ROOT", str(tmp_path))  # no stored traffic
+    line = {"value": 1000.0, "ms_per_step": 2000.0, "mfma_util_pct": 30.0, "steps": 3,
+            "kernels_from": "one untimed step",
+            "kernels": {"ffn1": {"launches": 492, "total_ms_per_step": 700.0, "avg_ms": 1.4,
+                                 "tflops": 850.0, "gbs": 1400.0}},
+            "roofline": {"kernel": "ffn1", "achieved": 845.0, "peak": 2516.6,
+                         "unit": "TFLOP/s", "frac": 845.0 / 2516.6, "avg_launch_ms": 1.48}}
+    path = tmp_path / "bench.json"
+    path.write_text(json.dumps(line))
+    md = P.roofline_markdown(str(path), "bge", "python bench.py")
+    row = [l for l in md.splitlines() if l.startswith("| ffn1 ")][0]
+    assert row.split("|")[2].strip() == "492"  # launches of the one step
+    assert "frac 0.336" in md
+    assert f"{100 * 850.0 / 2516.6:.1f}" in row
+
+
+def test_bench_refuses_more_than_one_gpu(capsys):
+    assert bench.main(["--gpus", "2"]) == 2
+    out = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
+    assert "one GPU" in out["error"]
