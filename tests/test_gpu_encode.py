@@ -265,21 +265,23 @@ def test_profile_select_times_only_the_selected_class():
         S._check(S.lib().surge_profile_select(enc.handle, 1 << len(S.KERNEL_NAMES)))
 
 
-def test_bge_texts_at_the_position_limit():
-    """bge shapes end to end with texts of the maximum length (every one of
-    the 512 learned positions, 16 key blocks of attention) next to one- and
-    two-token texts, an empty partition and a 32/33-token block boundary,
-    every text against the oracle."""
+@pytest.mark.parametrize("name", ["bge", "minilm", "large"])
+def test_texts_at_the_position_limit(name):
+    """Each encoder shape end to end with texts of the maximum length (every
+    learned position; 16 key blocks of attention for bge and large) next to
+    one- and two-token texts, an empty partition and a 32/33-token block
+    boundary, every text against the oracle."""
     torch = torch_cuda()
-    spec = W.WORKLOADS["bge"]
+    spec = W.WORKLOADS[name]
     sh = spec.encoder
-    lengths = [sh.max_positions, 1, sh.max_positions - 1, 2, 300, 33, 32, sh.max_positions]
+    P = sh.max_positions
+    lengths = [P, 1, P - 1, 2, min(300, P - 3), 33, 32, P]
     wl = W.workload_from_lengths(spec, [3, 0, 4, 1], lengths, seed=5)
     weights = W.make_weights(sh, seed=2)
-    print(f"[bge max length] lengths={lengths}", flush=True)
+    print(f"[{name} max length] lengths={lengths}", flush=True)
     enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 12)
     got, nsb = _encode_all(torch, enc, wl, sh.d_model, 3, 0)
     enc.close()
     assert not np.isnan(got).any()
     ref = _oracle_rows(spec, weights, wl, range(wl.n_texts))
-    assert_parity(got, ref, "bge")
+    assert_parity(got, ref, name)
