@@ -60,29 +60,58 @@ def encoder_flops(shape: W.EncoderShape, lengths: np.ndarray) -> float:
     return float(shape.n_layers * (2.0 * L * (4 * d * d + 2 * d * f) + 4.0 * d * L * L).sum())
 
 
-def cpu_baseline(spec, wl, weights, budget_s: float):
-    """The oracle, as it stands, on the first texts of SuperBatch 0."""
-    from oracle import encoder as E
+# Fixed prefix of SuperBatch 0 timed on the host per workload (texts).
+CPU_SAMPLE = {"tiny": 1000, "minilm": 2000, "minilm_heavy": 2000, "bge": 1000, "bge_s1": 1000,
+              "large": 200}
+
+
+def host_description():
+    """What the CPU baseline ran on: logical CPUs, the CPU model and the
+    NumPy BLAS build with the thread count it uses."""
+    info = {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0))}
+    try:
+        with open("/proc/cpuinfo") as f:
+            info["cpu_model"] = next((l.split(":", 1)[1].strip() for l in f
+                                      if l.startswith("model name")), None)
+    except OSError:
+        info["cpu_model"] = None
+    try:
+        blas = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        info["numpy_blas"] = f"{blas.get('name')} {blas.get('version')}"
+    except Exception:
+        info["numpy_blas"] = None
     try:
         from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        pools = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        info["blas_threads"] = max([p.get("num_threads", 1) for p in pools] + [1])
+        info["blas_runtime"] = ", ".join(f"{p.get('internal_api')} {p.get('version')} "
+                                         f"({p.get('architecture')})" for p in pools) or None
     except Exception:
-        cores = os.cpu_count() or 1
+        info["blas_threads"] = None
+        info["blas_runtime"] = None
+    return info
+
+
+def cpu_baseline(spec, wl, weights, n_sample: int, n_sb0: int):
+    """The float32 oracle, as it stands, on the first n_sample texts of
+    SuperBatch 0 (one text at a time, every BLAS thread of the host)."""
+    from oracle import encoder as E
+    host = host_description()
     sh = spec.encoder
-    w64 = E.as_f64(weights)
-    n = 0
-    toks = 0
+    w32 = E.as_f32(weights)
+    n = min(n_sample, n_sb0, wl.n_texts)
+    toks = int(wl.cu_seqlens[n] - wl.cu_seqlens[0])
     t0 = time.perf_counter()
-    while time.perf_counter() - t0 < budget_s and n < wl.n_texts:
-        ids = wl.tokens[wl.cu_seqlens[n]:wl.cu_seqlens[n + 1]]
-        E.encode_text(w64, sh.n_layers, sh.n_heads, ids, sh.ln_eps)
-        toks += len(ids)
-        n += 1
+    E.encode_texts(w32, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, range(n), sh.ln_eps)
     dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "texts/s", "cores": int(cores), "kind": "oracle",
+    flops = encoder_flops(sh, wl.lengths[:n])
+    return {"value": n / dt, "unit": "texts/s", "cores": host["blas_threads"] or host["nproc"],
+            "kind": "oracle",
             "sample": f"first {n} texts ({toks} tokens) of SuperBatch 0 of the same workload, "
-                      f"fp64 NumPy oracle, one text at a time, {dt:.1f} s",
-            "tokens_per_s": toks / dt}
+                      f"float32 NumPy oracle, one text at a time, {dt:.1f} s",
+            "tokens_per_s": toks / dt, "gflops": flops / dt / 1e9,
+            "extrapolated_full_workload_s": dt * wl.n_texts / n,
+            "host": host}
 
 
 def blas_reference(spec, wl, iters: int = 20):
@@ -141,7 +170,8 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="bge", choices=sorted(W.WORKLOADS))
     ap.add_argument("--chunk-tokens", type=int, default=1 << 20)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-texts", type=int, default=0,
+                    help="texts of the CPU-oracle sample (default: the workload's fixed prefix)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-kernel-events", action="store_true")
     ap.add_argument("--no-stream", action="store_true",
@@ -303,7 +333,10 @@ def main(argv=None):
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(spec, wl, weights, args.cpu_seconds)
+        sbs, _ = S.surge_plan(wl.part_offsets, spec.b_min, spec.n_max)
+        n_sb0 = int(sbs[0]["text_end"] - sbs[0]["text_begin"])
+        cpu = cpu_baseline(spec, wl, weights, args.cpu_texts or CPU_SAMPLE[args.workload], n_sb0)
+        print(f"[bench] cpu baseline done", file=sys.stderr, flush=True)
 
     line = {
         "metric": METRIC,

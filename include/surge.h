@@ -27,7 +27,11 @@
  *     a call that returns an error has written no output byte.
  *   - Calls return SURGE_OK or an error code; surge_last_error() gives a
  *     message (thread-local, valid until the next call on that thread).
- *   - An encoder is not thread-safe: use one encoder per host thread.
+ *   - An encoder is not thread-safe: use one encoder per host thread.  Its
+ *     device workspace is shared by every call, so each encode call first
+ *     makes its stream(s) wait for the previous call's work (on whatever
+ *     stream that ran): calls on different streams are ordered, never
+ *     overlapped, without any host synchronisation.
  */
 #ifndef SURGE_H_
 #define SURGE_H_
@@ -52,6 +56,10 @@ typedef int32_t surge_status;
 #define SURGE_POLICY_LITERAL 1 /* Alg. 1 as printed: append, then flush on
                                   total >= cap or total >= b_min */
 
+/* Element type of the host weight arrays given to surge_encoder_create. */
+#define SURGE_WEIGHTS_F32 0  /* IEEE float32 */
+#define SURGE_WEIGHTS_BF16 1 /* bfloat16 bit patterns (uint16_t), e.g. a bf16 checkpoint */
+
 /* Shape of a post-LN BERT-style encoder.  d_model % n_heads == 0 and
  * d_model / n_heads is 32 or 64; d_model and d_ff are multiples of 128. */
 typedef struct surge_encoder_desc {
@@ -62,7 +70,7 @@ typedef struct surge_encoder_desc {
   int32_t vocab_size;
   int32_t max_positions; /* longest text, in tokens */
   float ln_eps;          /* LayerNorm epsilon (1e-12 for BERT) */
-  int32_t reserved;      /* must be 0 */
+  int32_t weight_dtype;  /* SURGE_WEIGHTS_F32 or SURGE_WEIGHTS_BF16 */
 } surge_encoder_desc;
 
 /* One bound of a SuperBatch (Alg. 1, Flush: (start, end, key)): texts
@@ -129,23 +137,44 @@ surge_status surge_validate_superbatch(const surge_encoder_desc* desc, int64_t n
                                        float* const* h_part_out, int32_t n_parts);
 
 /*
+ * The host-side argument check of the whole-input entry points
+ * (surge_encode_all, surge_encode_all_streamed), exposed on its own (pure
+ * host code, no GPU needed).  Plans the input with surge_plan(part_offsets,
+ * n_parts, b_min, n_max, policy) and checks: part_offsets[n_parts] =
+ * n_texts; cu_seqlens[0] = 0 and every text length in [1,
+ * desc->max_positions]; every SuperBatch of the plan holds fewer than 2^31
+ * tokens; part_out[p] is non-NULL for every non-empty partition.  The total
+ * token count is not capped (offsets are int64 throughout).  Optionally
+ * returns the plan's SuperBatch count and its largest SuperBatch in texts
+ * and in tokens (any pointer may be NULL).
+ */
+surge_status surge_validate_input(const surge_encoder_desc* desc, int64_t n_texts,
+                                  const int64_t* h_cu_seqlens, const int64_t* h_part_offsets,
+                                  int32_t n_parts, int64_t b_min, int64_t n_max, int32_t policy,
+                                  float* const* h_part_out, int64_t* n_superbatches,
+                                  int64_t* max_sb_texts, int64_t* max_sb_tokens);
+
+/*
  * Create an encoder on the current HIP device.
  *
- * host_weights: n_weights = 4 + 12 * n_layers host fp32 arrays, row-major, in
+ * host_weights: n_weights = 4 + 12 * n_layers host arrays of
+ *   desc->weight_dtype elements (float32, or bf16 bit patterns), row-major, in
  *   this order: word_emb [vocab, d], pos_emb [max_positions, d], ln_e gamma
  *   [d], ln_e beta [d]; then per layer: W_qkv [d, 3d], b_qkv [3d], W_o [d, d],
  *   b_o [d], ln1 gamma [d], ln1 beta [d], W_1 [d, d_ff], b_1 [d_ff],
  *   W_2 [d_ff, d], b_2 [d], ln2 gamma [d], ln2 beta [d].  Matrices are
  *   [in, out] (y = x W + b); W_qkv holds Q | K | V as column blocks, head h
  *   owning columns [h*dh, (h+1)*dh) of each block.  Matrices and embedding
- *   tables are rounded to bf16 (nearest, ties to even) on the device;
- *   biases and LayerNorm parameters stay fp32.  The caller may free the
- *   host arrays when the call returns.
+ *   tables are rounded to bf16 (nearest, ties to even; bf16 input is used
+ *   as is); biases and LayerNorm parameters are kept in fp32 (bf16 input is
+ *   widened exactly).  float32 arrays holding bf16-representable values and
+ *   the bf16 arrays of the same values give bit-identical encoders.  The
+ *   caller may free the host arrays when the call returns.
  * max_tokens_per_chunk: size of the activation workspace in tokens (>=
  *   max_positions).  A SuperBatch with more tokens is encoded in several
  *   chunks cut at text boundaries; results do not depend on the cut.
  */
-surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* const* host_weights,
+surge_status surge_encoder_create(const surge_encoder_desc* desc, const void* const* host_weights,
                                   int32_t n_weights, int64_t max_tokens_per_chunk,
                                   surge_encoder** out);
 
@@ -216,6 +245,14 @@ typedef struct surge_stream_stats {
    * share of the I/O time that did not extend the wall time (clamped to
    * [0, 1]). */
   double rho_measured;
+  /* Device staging memory the call allocated: two token buffers for the
+   * plan's largest SuperBatch in tokens and (overlap 0 and 1) two embedding
+   * buffers for its largest SuperBatch in texts, i.e. twice Lemma 1's
+   * M(S) = S L + 4 S d with the text part as int32 token IDs (Sec. 4.3),
+   * bounded through S <= B_min - 1 + n_max and, with the cap, S <= n_max. */
+  int64_t staging_bytes;
+  int64_t max_sb_texts;
+  int64_t max_sb_tokens;
 } surge_stream_stats;
 
 /*
@@ -258,8 +295,9 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
                                        double* h_sb_times, int64_t sb_times_cap,
                                        surge_stream_stats* stats);
 
-/* Synchronise `hip_stream`, then report deferred device-side errors (a token
- * ID outside the vocabulary -> SURGE_ERR_INVALID_ARGUMENT) and clear them. */
+/* Synchronise `hip_stream` and the encoder's last enqueued call, then report
+ * deferred device-side errors (a token ID outside the vocabulary ->
+ * SURGE_ERR_INVALID_ARGUMENT) and clear them. */
 surge_status surge_check(surge_encoder* enc, void* hip_stream);
 
 /*

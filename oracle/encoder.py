@@ -1,6 +1,14 @@
 """Oracle: the per-text encoder forward, pooling, normalisation and placement.
 
-TEST INFRASTRUCTURE ONLY (see the package docstring).  Float64 NumPy.
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+Precision.  Every function computes in the floating-point type of the
+weights it is given: ``as_dtype(weights, np.float32)`` gives the oracle the
+GPU path is held to (plain float32 NumPy, BLAS sgemm for the products,
+``scipy.special.erf`` for GELU); ``as_dtype(weights, np.float64)`` gives its
+float64 twin, which pins the float32 results (they agree to cosine
+>= 1 - 1e-9 and max-abs <= 1e-5 per component) and is the form compared
+with the library encoder and the brute-force references.
 
 What is computed, and where it comes from:
 
@@ -31,6 +39,7 @@ blocks of width d, head h owns columns [h*dh, (h+1)*dh) in each block.
 """
 from __future__ import annotations
 
+import math
 from typing import Dict, List, Sequence
 
 import numpy as np
@@ -39,8 +48,19 @@ from scipy.special import erf
 L2_EPS = 1e-12
 
 
+def as_dtype(weights: Dict[str, np.ndarray], dtype) -> Dict[str, np.ndarray]:
+    """The weights as arrays of ``dtype`` (np.float32: the oracle; np.float64:
+    its twin).  The oracle's arithmetic then runs in that type: every scalar
+    it mixes in is a Python float, which never widens an array."""
+    return {k: np.asarray(v, dtype=dtype) for k, v in weights.items()}
+
+
+def as_f32(weights: Dict[str, np.ndarray]) -> Dict[str, np.ndarray]:
+    return as_dtype(weights, np.float32)
+
+
 def as_f64(weights: Dict[str, np.ndarray]) -> Dict[str, np.ndarray]:
-    return {k: np.asarray(v, dtype=np.float64) for k, v in weights.items()}
+    return as_dtype(weights, np.float64)
 
 
 def layer_norm(x: np.ndarray, gamma: np.ndarray, beta: np.ndarray, eps: float) -> np.ndarray:
@@ -52,7 +72,7 @@ def layer_norm(x: np.ndarray, gamma: np.ndarray, beta: np.ndarray, eps: float) -
 
 def gelu(z: np.ndarray) -> np.ndarray:
     """Exact GELU: z * Phi(z) = 0.5 z (1 + erf(z / sqrt 2))."""
-    return 0.5 * z * (1.0 + erf(z / np.sqrt(2.0)))
+    return 0.5 * z * (1.0 + erf(z / math.sqrt(2.0)))
 
 
 def linear(x: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
@@ -81,7 +101,7 @@ def self_attention(qkv: np.ndarray, n_heads: int) -> np.ndarray:
     out = np.empty((L, d), dtype=qkv.dtype)
     for h in range(n_heads):
         cols = slice(h * dh, (h + 1) * dh)
-        s = q[:, cols] @ k[:, cols].T / np.sqrt(dh)
+        s = q[:, cols] @ k[:, cols].T / math.sqrt(dh)
         out[:, cols] = softmax_rows(s) @ v[:, cols]
     return out
 
@@ -124,7 +144,7 @@ def mean_pool_l2(x: np.ndarray) -> np.ndarray:
 
 def encode_text(w: Dict[str, np.ndarray], n_layers: int, n_heads: int,
                 ids: np.ndarray, eps: float = 1e-12) -> np.ndarray:
-    """The embedding of one text (float64 [d])."""
+    """The embedding of one text ([d], in the weights' floating-point type)."""
     return mean_pool_l2(hidden_states(w, n_layers, n_heads, ids, eps))
 
 
@@ -133,7 +153,7 @@ def encode_texts(w: Dict[str, np.ndarray], n_layers: int, n_heads: int,
                  indices: Sequence[int], eps: float = 1e-12) -> np.ndarray:
     """Embeddings [len(indices), d] of the chosen texts, each encoded alone."""
     d = w["word_emb"].shape[1]
-    out = np.empty((len(indices), d), dtype=np.float64)
+    out = np.empty((len(indices), d), dtype=w["word_emb"].dtype)
     for j, i in enumerate(indices):
         ids = tokens[int(cu_seqlens[i]):int(cu_seqlens[i + 1])]
         out[j] = encode_text(w, n_layers, n_heads, ids, eps)
@@ -154,7 +174,7 @@ def encode_workload(w: Dict[str, np.ndarray], n_layers: int, n_heads: int,
     """Per-partition outputs: out[p][i - part_offsets[p]] = e_i for every text i."""
     d = w["word_emb"].shape[1]
     n_parts = len(part_offsets) - 1
-    out = [np.empty((int(part_offsets[p + 1] - part_offsets[p]), d))
+    out = [np.empty((int(part_offsets[p + 1] - part_offsets[p]), d), dtype=w["word_emb"].dtype)
            for p in range(n_parts)]
     n = len(cu_seqlens) - 1
     for i in range(n):

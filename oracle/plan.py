@@ -201,7 +201,26 @@ def ffd_pack(part_sizes: Sequence[int], capacity: int) -> List[List[int]]:
     return bins
 
 
-def superbatch_memory(n_texts: int, n_tokens: int, d: int, bytes_per_token: int = 4) -> int:
-    """Lemma 1's data-resident size of a SuperBatch, M(S) = S L + 4 S d bytes,
-    with the text part counted as its token IDs (bytes_per_token each)."""
-    return n_tokens * bytes_per_token + 4 * n_texts * d
+def superbatch_memory(n_texts: int, mean_text_bytes: float, d: int) -> float:
+    """Lemma 1 (Sec. 4.3, "SuperBatch memory"): the data-resident size of a
+    SuperBatch of S texts of average size L bytes with fp32 embeddings of
+    width d is M(S) = S L + 4 S d bytes (the raw texts plus the [S, d]
+    embedding matrix)."""
+    return n_texts * mean_text_bytes + 4 * n_texts * d
+
+
+def device_superbatch_memory(n_texts: int, n_tokens: int, d: int) -> int:
+    """Lemma 1's M(S) for a SuperBatch held on the device as packed int32
+    token IDs: the text part is 4 bytes per token, i.e. L = 4 n_tokens / S."""
+    return 4 * n_tokens + 4 * n_texts * d
+
+
+def largest_superbatch_bound(b_min: int, n_big: int, cap: int = 0, policy: int = R2) -> int:
+    """Lemma 1's bound on the texts of one SuperBatch: the buffer holds less
+    than B_min texts before the arriving partition (at most n_max texts) is
+    appended, so S <= B_min - 1 + n_max; with the pre-append cap of the R2
+    reading every SuperBatch also holds at most ``cap`` texts."""
+    bound = b_min - 1 + n_big
+    if policy == R2 and cap > 0:
+        bound = min(bound, cap)
+    return bound

@@ -65,6 +65,11 @@ struct surge_encoder {
   uint64_t* d_dst = nullptr;   // [max_tokens]
   uint32_t* d_items = nullptr; // [max_tokens] attention work items
   int* d_err = nullptr;
+  int n_cus = 0;  // compute units of the device (GEMM grid size)
+  // The workspace is shared by every call: each call's stream waits for the
+  // previous call's last work, which this event marks.
+  hipEvent_t last_use = nullptr;
+  bool last_use_recorded = false;
   // pinned staging ring for chunk metadata
   void* staging[kStagingSlots] = {};
   hipEvent_t staging_ev[kStagingSlots] = {};
@@ -100,6 +105,7 @@ void free_encoder(surge_encoder* e) {
     if (e->staging[i]) hipHostFree(e->staging[i]);
   }
   for (hipEvent_t ev : e->prof_events) hipEventDestroy(ev);
+  if (e->last_use) hipEventDestroy(e->last_use);
   if (e->wblock) hipFree(e->wblock);
   if (e->wsblock) hipFree(e->wsblock);
   delete e;
@@ -142,6 +148,19 @@ surge_status prof_end(surge_encoder* e, hipStream_t s, int ev, int kind, double 
     st_ = prof_end(e, stream, ev_, kind, flops, bytes);              \
     if (st_ != SURGE_OK) return st_;                                 \
   } while (0)
+
+// Order a call after the encoder's previous one: `stream` waits for the
+// event recorded at the end of that call (a no-op before the first call).
+surge_status begin_call(surge_encoder* e, hipStream_t stream) {
+  if (e->last_use_recorded) HIP_TRY(hipStreamWaitEvent(stream, e->last_use, 0));
+  return SURGE_OK;
+}
+
+surge_status end_call(surge_encoder* e, hipStream_t stream) {
+  HIP_TRY(hipEventRecord(e->last_use, stream));
+  e->last_use_recorded = true;
+  return SURGE_OK;
+}
 
 // Encode texts [0, n_texts) of a validated SuperBatch whose row pointers are
 // in e->h_dst.  cu is SuperBatch-local host int64.
@@ -200,6 +219,7 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
       const LayerWeights& w = e->layers[l];
       const LayerWeights* pw = l > 0 ? &e->layers[l - 1] : nullptr;
       LinearExtra xq;  // QKV: LN2 of the previous layer folded in (layer 0: plain)
+      xq.n_cus = e->n_cus;
       xq.rows_in = e->RX;
       xq.col_s = w.sqkv;
       LAUNCH(SURGE_KERNEL_QKV, 2.0 * Td * d * 3 * d, 2.0 * (Td * d + 3.0 * d * d + Td * 3 * d),
@@ -208,6 +228,7 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
       LAUNCH(SURGE_KERNEL_ATTN, 4.0 * d * sumL2, 2.0 * Td * 4 * d,
              launch_attention(e->QKV, e->CTX, e->d_cu, e->d_items, n_items, D.n_heads, dh, stream));
       LinearExtra xo;  // O-proj + residual (LN2 of the previous layer applied to it)
+      xo.n_cus = e->n_cus;
       xo.rows_in = e->RX;
       xo.stats_out = e->SY;
       xo.gamma = pw ? pw->ln2g : nullptr;
@@ -218,11 +239,13 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
       LAUNCH(SURGE_KERNEL_LN1, 0.0, Td * (8.0 * parts + 8.0),
              launch_ln_rows(e->SY, parts, T, D.ln_eps, e->RY, stream));
       LinearExtra x1;  // FFN1: LN1 folded in
+      x1.n_cus = e->n_cus;
       x1.rows_in = e->RY;
       x1.col_s = w.s1;
       LAUNCH(SURGE_KERNEL_FFN1, 2.0 * Td * d * f, 2.0 * (Td * d + (double)d * f + Td * f),
              launch_linear(e->Y, w.w1, w.b1, nullptr, e->H, T, f, d, EPI_FOLD_GELU, x1, stream));
       LinearExtra x2;  // FFN2 + residual LN1(Y)
+      x2.n_cus = e->n_cus;
       x2.rows_in = e->RY;
       x2.stats_out = e->SX;
       x2.gamma = w.ln1g;
@@ -291,7 +314,7 @@ surge_status make_plan(const int64_t* part_offsets, int32_t n_parts, int64_t b_m
 
 extern "C" {
 
-surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* const* host_weights,
+surge_status surge_encoder_create(const surge_encoder_desc* desc, const void* const* host_weights_in,
                                   int32_t n_weights, int64_t max_tokens_per_chunk,
                                   surge_encoder** out) {
   clear_error();
@@ -301,11 +324,11 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   if (st != SURGE_OK) return st;
   const surge_encoder_desc D = *desc;
   const int64_t expect = 4 + 12 * (int64_t)D.n_layers;
-  if (!host_weights || n_weights != expect)
+  if (!host_weights_in || n_weights != expect)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "expected %lld weight arrays, got %d",
                 (long long)expect, n_weights);
   for (int i = 0; i < n_weights; ++i)
-    if (!host_weights[i]) return fail(SURGE_ERR_INVALID_ARGUMENT, "weight %d is NULL", i);
+    if (!host_weights_in[i]) return fail(SURGE_ERR_INVALID_ARGUMENT, "weight %d is NULL", i);
   if (max_tokens_per_chunk < D.max_positions || max_tokens_per_chunk > (int64_t)1 << 25)
     return fail(SURGE_ERR_INVALID_ARGUMENT,
                 "max_tokens_per_chunk=%lld outside [max_positions, 2^25]",
@@ -321,6 +344,32 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   }
 
   const int64_t d = D.d_model, f = D.d_ff, V = D.vocab_size, P = D.max_positions;
+  // Element counts of the weight arrays, in the fixed order.
+  std::vector<int64_t> counts = {V * d, P * d, d, d};
+  for (int l = 0; l < D.n_layers; ++l) {
+    const int64_t per[12] = {d * 3 * d, 3 * d, d * d, d, d, d, d * f, f, f * d, d, d, d};
+    counts.insert(counts.end(), per, per + 12);
+  }
+  // bf16 input: every array widened exactly to float32 first, so both input
+  // types go through the same rounding and folding below.
+  std::vector<std::vector<float>> widened;
+  std::vector<const float*> hw((size_t)n_weights);
+  if (D.weight_dtype == SURGE_WEIGHTS_BF16) {
+    widened.resize((size_t)n_weights);
+    for (int i = 0; i < n_weights; ++i) {
+      const uint16_t* src = (const uint16_t*)host_weights_in[i];
+      std::vector<float>& dst = widened[(size_t)i];
+      dst.resize((size_t)counts[(size_t)i]);
+      for (int64_t k = 0; k < counts[(size_t)i]; ++k) {
+        const uint32_t bits = (uint32_t)src[k] << 16;
+        memcpy(&dst[(size_t)k], &bits, 4);
+      }
+      hw[(size_t)i] = dst.data();
+    }
+  } else {
+    for (int i = 0; i < n_weights; ++i) hw[(size_t)i] = (const float*)host_weights_in[i];
+  }
+  const float* const* host_weights = hw.data();
   // Device weight block layout (byte offsets, 256-aligned pieces).
   std::vector<size_t> offs;
   size_t total = 0;
@@ -501,6 +550,14 @@ surge_status surge_encoder_create(const surge_encoder_desc* desc, const float* c
   if (err != hipSuccess)
     return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipMemset failed: %s", hipGetErrorString(err)));
 
+  err = hipDeviceGetAttribute(&e->n_cus, hipDeviceAttributeMultiprocessorCount, e->device);
+  if (err != hipSuccess)
+    return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipDeviceGetAttribute failed: %s",
+                             hipGetErrorString(err)));
+  err = hipEventCreateWithFlags(&e->last_use, hipEventDisableTiming);
+  if (err != hipSuccess)
+    return cleanup_fail(fail(SURGE_ERR_DEVICE, "hipEventCreate failed: %s", hipGetErrorString(err)));
+
   e->staging_bytes = align_up((size_t)(T + 1) * 4, 16) + (size_t)T * 8 + (size_t)T * 4;
   for (int i = 0; i < kStagingSlots; ++i) {
     err = hipHostMalloc(&e->staging[i], e->staging_bytes, hipHostMallocDefault);
@@ -543,8 +600,13 @@ surge_status surge_encode_superbatch(surge_encoder* enc, int64_t n_texts, int64_
   if (n_texts == 0) return SURGE_OK;
   HIP_TRY(hipSetDevice(enc->device));
   surge_encoder* e = enc;
+  const hipStream_t stream = (hipStream_t)hip_stream;
   resolve_rows(e, n_texts, h_segs, n_segs, h_part_out);
-  return encode_chunks(e, n_texts, d_token_ids, h_cu_seqlens, (hipStream_t)hip_stream);
+  st = begin_call(e, stream);
+  if (st != SURGE_OK) return st;
+  st = encode_chunks(e, n_texts, d_token_ids, h_cu_seqlens, stream);
+  if (st != SURGE_OK) return st;
+  return end_call(e, stream);
 }
 
 surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t* d_token_ids,
@@ -554,29 +616,27 @@ surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t
                               void* hip_stream) {
   clear_error();
   if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
-  if (!h_part_offsets || !h_cu_seqlens || !h_part_out)
-    return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL host array");
-  if (n_parts < 0 || h_part_offsets[n_parts] != n_texts)
-    return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts] != n_texts");
   if (first_sb < 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "first_sb < 0");
+  // Validate the whole input once (int64 offsets, no cap on the total token
+  // count), then every SuperBatch of the plan is consistent.
+  surge_status st = surge_validate_input(&enc->desc, n_texts, h_cu_seqlens, h_part_offsets,
+                                         n_parts, b_min, n_max, policy, h_part_out, nullptr,
+                                         nullptr, nullptr);
+  if (st != SURGE_OK) return st;
   Plan ctx;
   int64_t ns = 0;
-  surge_status st = make_plan(h_part_offsets, n_parts, b_min, n_max, policy, &ctx, &ns);
+  st = make_plan(h_part_offsets, n_parts, b_min, n_max, policy, &ctx, &ns);
   if (st != SURGE_OK) return st;
   if (n_superbatches) *n_superbatches = ns;
-  // Validate the whole input once, then every SuperBatch is consistent.
-  std::vector<int64_t> sizes((size_t)n_parts);
-  for (int32_t p = 0; p < n_parts; ++p) sizes[p] = h_part_offsets[p + 1] - h_part_offsets[p];
-  st = surge_validate_superbatch(&enc->desc, n_texts, h_cu_seqlens[n_texts], h_cu_seqlens,
-                                 ctx.segs.data(), (int64_t)ctx.segs.size(), sizes.data(),
-                                 h_part_out, n_parts);
-  if (st != SURGE_OK) return st;
   st = check_alignment((int64_t)ctx.segs.size(), ctx.segs.data(), h_part_out);
   if (st != SURGE_OK) return st;
   if (n_texts > 0 && !d_token_ids) return fail(SURGE_ERR_INVALID_ARGUMENT, "token_ids is NULL");
   if (n_texts == 0) return SURGE_OK;
   HIP_TRY(hipSetDevice(enc->device));
   surge_encoder* e = enc;
+  const hipStream_t stream = (hipStream_t)hip_stream;
+  st = begin_call(e, stream);
+  if (st != SURGE_OK) return st;
   std::vector<int64_t> lcu;
   for (int64_t k = first_sb; k < ns; ++k) {
     const PlanSB& sb = ctx.sbs[(size_t)k];
@@ -593,10 +653,10 @@ surge_status surge_encode_all(surge_encoder* enc, int64_t n_texts, const int32_t
       for (int64_t j = 0; j < g.count; ++j)
         e->h_dst[(size_t)(g.first_text - sb.text_begin + j)] = (uint64_t)(uintptr_t)(rb + j * d);
     }
-    st = encode_chunks(e, S, d_token_ids + base, lcu.data(), (hipStream_t)hip_stream);
+    st = encode_chunks(e, S, d_token_ids + base, lcu.data(), stream);
     if (st != SURGE_OK) return st;
   }
-  return SURGE_OK;
+  return end_call(e, stream);
 }
 
 surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
@@ -609,28 +669,24 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   clear_error();
   if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
   if (!h_part_offsets || !h_cu_seqlens) return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL host array");
-  if (n_parts < 0 || h_part_offsets[n_parts] != n_texts)
-    return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts] != n_texts");
+  if (n_parts < 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "n_parts < 0");
   if (overlap < 0 || overlap > 2) return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap=%d", overlap);
   if (overlap == 1 && compute_stream == copy_stream)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "overlap needs two different streams");
   if (h_sb_times == nullptr && sb_times_cap != 0)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "sb_times_cap > 0 with NULL h_sb_times");
-  Plan plan;
-  int64_t ns = 0;
-  surge_status st = make_plan(h_part_offsets, n_parts, b_min, n_max, policy, &plan, &ns);
-  if (st != SURGE_OK) return st;
   const int64_t d = enc->desc.d_model;
   // Validate once against per-partition views of h_out (never dereferenced).
-  std::vector<int64_t> sizes((size_t)n_parts);
   std::vector<float*> views((size_t)n_parts);
-  for (int32_t p = 0; p < n_parts; ++p) {
-    sizes[p] = h_part_offsets[p + 1] - h_part_offsets[p];
-    views[p] = h_out ? h_out + h_part_offsets[p] * d : nullptr;
-  }
-  st = surge_validate_superbatch(&enc->desc, n_texts, h_cu_seqlens[n_texts], h_cu_seqlens,
-                                 plan.segs.data(), (int64_t)plan.segs.size(), sizes.data(),
-                                 views.data(), n_parts);
+  for (int32_t p = 0; p < n_parts; ++p) views[p] = h_out ? h_out + h_part_offsets[p] * d : nullptr;
+  int64_t max_tok = 0, max_txt = 0;
+  surge_status st = surge_validate_input(&enc->desc, n_texts, h_cu_seqlens, h_part_offsets, n_parts,
+                                         b_min, n_max, policy, views.data(), nullptr, &max_txt,
+                                         &max_tok);
+  if (st != SURGE_OK) return st;
+  Plan plan;
+  int64_t ns = 0;
+  st = make_plan(h_part_offsets, n_parts, b_min, n_max, policy, &plan, &ns);
   if (st != SURGE_OK) return st;
   if (stats) memset(stats, 0, sizeof(*stats));
   if (n_texts == 0) return SURGE_OK;
@@ -660,11 +716,6 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
     d_out_mapped = (float*)a0.devicePointer;
   }
 
-  int64_t max_tok = 0, max_txt = 0;
-  for (const PlanSB& sb : plan.sbs) {
-    max_tok = std::max(max_tok, h_cu_seqlens[sb.text_end] - h_cu_seqlens[sb.text_begin]);
-    max_txt = std::max(max_txt, sb.text_end - sb.text_begin);
-  }
   // Staging buffers and events, released on every exit path after both
   // streams have drained.
   struct Res {
@@ -684,9 +735,20 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
   } r;
   r.s1 = cs;
   r.s2 = xs;
+  // Lemma 1's staging: per buffer the largest SuperBatch's tokens (int32)
+  // and, unless zero copy, its [S, d] fp32 embeddings.
+  const int64_t staging =
+      2 * (std::max<int64_t>(max_tok, 1) * 4 + (zero_copy ? 0 : max_txt * d * 4));
   for (int i = 0; i < 2; ++i) {
     HIP_TRY(hipMalloc(&r.tok[i], (size_t)std::max<int64_t>(max_tok, 1) * 4));
     if (!zero_copy) HIP_TRY(hipMalloc(&r.out[i], (size_t)max_txt * d * 4));
+  }
+  // Ordered after the encoder's previous call, on both streams.
+  st = begin_call(e, cs);
+  if (st != SURGE_OK) return st;
+  if (xs != cs) {
+    st = begin_call(e, xs);
+    if (st != SURGE_OK) return st;
   }
   // Six events per SuperBatch: upload, encode and download start / end.
   r.ev.resize((size_t)ns * 6, nullptr);
@@ -755,6 +817,8 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
       }
     }
   }
+  st = end_call(e, xs);  // the copy stream ends last (it waits for the last encode)
+  if (st != SURGE_OK) return st;
   HIP_TRY(hipStreamSynchronize(cs));
   HIP_TRY(hipStreamSynchronize(xs));
   // Timing summary.
@@ -790,6 +854,9 @@ surge_status surge_encode_all_streamed(surge_encoder* enc, int64_t n_texts,
     stats->rho_measured =
         h2d_ms + d2h_ms > 0.0 ? std::min(1.0, std::max(0.0, 1.0 - exposed / (h2d_ms + d2h_ms)))
                               : 1.0;
+    stats->staging_bytes = staging;
+    stats->max_sb_texts = max_txt;
+    stats->max_sb_tokens = max_tok;
   }
   int flag = 0;
   HIP_TRY(hipMemcpy(&flag, e->d_err, sizeof(int), hipMemcpyDeviceToHost));
@@ -805,6 +872,7 @@ surge_status surge_check(surge_encoder* enc, void* hip_stream) {
   if (!enc) return fail(SURGE_ERR_INVALID_ARGUMENT, "encoder is NULL");
   HIP_TRY(hipSetDevice(enc->device));
   HIP_TRY(hipStreamSynchronize((hipStream_t)hip_stream));
+  if (enc->last_use_recorded) HIP_TRY(hipEventSynchronize(enc->last_use));
   int flag = 0;
   HIP_TRY(hipMemcpy(&flag, enc->d_err, sizeof(int), hipMemcpyDeviceToHost));
   if (flag) {

@@ -6,6 +6,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "internal.h"
@@ -54,7 +55,9 @@ surge_status validate_desc(const surge_encoder_desc* d) {
                 d->max_positions);
   if (!(d->ln_eps >= 0.0f) || !isfinite(d->ln_eps))
     return fail(SURGE_ERR_INVALID_ARGUMENT, "ln_eps must be finite and >= 0");
-  if (d->reserved != 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "reserved must be 0");
+  if (d->weight_dtype != SURGE_WEIGHTS_F32 && d->weight_dtype != SURGE_WEIGHTS_BF16)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "weight_dtype=%d is neither F32 (0) nor BF16 (1)",
+                d->weight_dtype);
   return SURGE_OK;
 }
 
@@ -245,6 +248,55 @@ surge_status surge_validate_superbatch(const surge_encoder_desc* desc, int64_t n
   if (t != n_texts)
     return fail(SURGE_ERR_INVALID_ARGUMENT, "segments cover %lld texts, expected %lld", (long long)t,
                 (long long)n_texts);
+  return SURGE_OK;
+}
+
+surge_status surge_validate_input(const surge_encoder_desc* desc, int64_t n_texts,
+                                  const int64_t* cu, const int64_t* part_offsets, int32_t n_parts,
+                                  int64_t b_min, int64_t n_max, int32_t policy,
+                                  float* const* part_out, int64_t* n_superbatches,
+                                  int64_t* max_sb_texts, int64_t* max_sb_tokens) {
+  clear_error();
+  surge_status st = validate_desc(desc);
+  if (st != SURGE_OK) return st;
+  if (!cu || !part_offsets) return fail(SURGE_ERR_INVALID_ARGUMENT, "NULL host array");
+  if (n_texts < 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "n_texts=%lld < 0", (long long)n_texts);
+  if (n_parts < 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "n_parts=%d < 0", n_parts);
+  if (part_offsets[n_parts] != n_texts)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "part_offsets[n_parts]=%lld != n_texts=%lld",
+                (long long)part_offsets[n_parts], (long long)n_texts);
+  if (cu[0] != 0) return fail(SURGE_ERR_INVALID_ARGUMENT, "cu_seqlens[0]=%lld != 0", (long long)cu[0]);
+  for (int64_t i = 0; i < n_texts; ++i) {
+    const int64_t L = cu[i + 1] - cu[i];
+    if (L < 1 || L > desc->max_positions)
+      return fail(SURGE_ERR_INVALID_ARGUMENT, "text %lld has length %lld outside [1, %d]",
+                  (long long)i, (long long)L, desc->max_positions);
+  }
+  // The plan (this also checks part_offsets, b_min and the policy).
+  struct Scan {
+    const int64_t* cu;
+    int64_t n = 0, max_texts = 0, max_tokens = 0;
+  } scan{cu};
+  auto on_sb = [](void* c, const PlanSB& s) {
+    Scan* q = (Scan*)c;
+    ++q->n;
+    q->max_texts = std::max(q->max_texts, s.text_end - s.text_begin);
+    q->max_tokens = std::max(q->max_tokens, q->cu[s.text_end] - q->cu[s.text_begin]);
+  };
+  int64_t ns = 0, ng = 0;
+  st = plan_superbatches(part_offsets, n_parts, b_min, n_max, policy, on_sb, nullptr, &scan, &ns,
+                         &ng);
+  if (st != SURGE_OK) return st;
+  if (scan.max_tokens > (int64_t)INT32_MAX)
+    return fail(SURGE_ERR_INVALID_ARGUMENT, "a SuperBatch holds %lld tokens (>= 2^31)",
+                (long long)scan.max_tokens);
+  if (n_texts > 0 && !part_out) return fail(SURGE_ERR_INVALID_ARGUMENT, "part_out is NULL");
+  for (int32_t p = 0; p < n_parts; ++p)
+    if (part_offsets[p + 1] > part_offsets[p] && !part_out[p])
+      return fail(SURGE_ERR_INVALID_ARGUMENT, "output of partition %d is NULL", p);
+  if (n_superbatches) *n_superbatches = ns;
+  if (max_sb_texts) *max_sb_texts = scan.max_texts;
+  if (max_sb_tokens) *max_sb_tokens = scan.max_tokens;
   return SURGE_OK;
 }
 

@@ -53,6 +53,7 @@ struct LinearExtra {
   const float* col_s = nullptr;      // [N] (FOLD)
   const float* gamma = nullptr;      // [N] (LNRES)
   const float* beta = nullptr;       // [N] (LNRES)
+  int n_cus = 0;                     // compute units of the device (0: query it)
 };
 hipError_t launch_linear(const uint16_t* X, const uint16_t* W, const float* bias, const uint16_t* R,
                          uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,

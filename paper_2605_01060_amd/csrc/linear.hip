@@ -543,11 +543,14 @@ hipError_t launch_tiles(const uint16_t* X, const uint16_t* W, const float* bias,
                         uint16_t* Y, int64_t M, int N, int K, int epi, const LinearExtra& ex,
                         hipStream_t stream) {
   if ((int64_t)BM * K * 2 > (int64_t)UINT32_MAX) return hipErrorInvalidValue;  // copy offsets
-  int dev = 0, cus = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e != hipSuccess) return e;
+  int cus = ex.n_cus;
+  if (cus <= 0) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+  }
   const int tiles_n = N / BN;
   const int64_t tiles_m = (M + BM - 1) / BM;
   const int n_tiles = (int)(tiles_m * tiles_n);

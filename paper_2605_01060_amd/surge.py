@@ -27,6 +27,9 @@ SURGE_ERR_INTERNAL = 5
 SURGE_POLICY_SPLIT = 0
 SURGE_POLICY_LITERAL = 1
 
+SURGE_WEIGHTS_F32 = 0
+SURGE_WEIGHTS_BF16 = 1
+
 KERNEL_NAMES = ["embed", "qkv", "attn", "oproj", "ln1", "ffn1", "ffn2", "ln2", "pool"]
 
 SEGMENT_DTYPE = np.dtype([("first_text", "<i8"), ("count", "<i8"), ("row_offset", "<i8"),
@@ -45,14 +48,16 @@ class EncoderDesc(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
                 ("n_heads", ctypes.c_int32), ("d_ff", ctypes.c_int32),
                 ("vocab_size", ctypes.c_int32), ("max_positions", ctypes.c_int32),
-                ("ln_eps", ctypes.c_float), ("reserved", ctypes.c_int32)]
+                ("ln_eps", ctypes.c_float), ("weight_dtype", ctypes.c_int32)]
 
 
 class StreamStats(ctypes.Structure):
     _fields_ = [("n_superbatches", ctypes.c_int64), ("total_ms", ctypes.c_double),
                 ("ttfo_ms", ctypes.c_double), ("enc_ms", ctypes.c_double),
                 ("h2d_ms", ctypes.c_double), ("d2h_ms", ctypes.c_double),
-                ("rho", ctypes.c_double), ("rho_measured", ctypes.c_double)]
+                ("rho", ctypes.c_double), ("rho_measured", ctypes.c_double),
+                ("staging_bytes", ctypes.c_int64), ("max_sb_texts", ctypes.c_int64),
+                ("max_sb_tokens", ctypes.c_int64)]
 
 
 class KernelStat(ctypes.Structure):
@@ -71,6 +76,7 @@ _SIGNATURES = {
     "surge_last_error": ([], ctypes.c_char_p),
     "surge_plan": ([_P, _I32, _I64, _I64, _I32, _P, _I64, _P, _P, _I64, _P], _I32),
     "surge_validate_superbatch": ([_P, _I64, _I64, _P, _P, _I64, _P, _P, _I32], _I32),
+    "surge_validate_input": ([_P, _I64, _P, _P, _I32, _I64, _I64, _I32, _P, _P, _P, _P], _I32),
     "surge_encoder_create": ([_P, _P, _I32, _I64, _P], _I32),
     "surge_encoder_destroy": ([_P], None),
     "surge_encoder_info": ([_P, _P, _P, _P], _I32),
@@ -176,8 +182,9 @@ def surge_plan(part_offsets, b_min: int, n_max: int = 0,
 
 
 def make_desc(n_layers, d_model, n_heads, d_ff, vocab_size, max_positions,
-              ln_eps=1e-12) -> EncoderDesc:
-    return EncoderDesc(n_layers, d_model, n_heads, d_ff, vocab_size, max_positions, ln_eps, 0)
+              ln_eps=1e-12, weight_dtype=SURGE_WEIGHTS_F32) -> EncoderDesc:
+    return EncoderDesc(n_layers, d_model, n_heads, d_ff, vocab_size, max_positions, ln_eps,
+                       weight_dtype)
 
 
 def segments_array(rows: Sequence[Tuple[int, int, int, int]]) -> np.ndarray:
@@ -200,9 +207,26 @@ def surge_validate_superbatch(desc: EncoderDesc, n_texts: int, n_tokens: int, cu
                                            segs.shape[0], psz, pout, sizes.shape[0])
 
 
+def surge_validate_input(desc: EncoderDesc, n_texts: int, cu_seqlens, part_offsets, b_min: int,
+                         n_max: int, policy: int, part_out_ptrs) -> Tuple[int, Dict[str, int]]:
+    """Status code of the whole-input check (does not raise) and, on success,
+    the plan's SuperBatch count and largest SuperBatch in texts and tokens."""
+    cu, pcu = _host(cu_seqlens, np.int64)
+    offs, poff = _host(part_offsets, np.int64)
+    outs, pout = _host(part_out_ptrs, np.uint64)
+    ns, mt, mk = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int64(0)
+    st = lib().surge_validate_input(ctypes.byref(desc), n_texts, pcu, poff, offs.shape[0] - 1,
+                                    b_min, n_max, policy, pout, ctypes.byref(ns),
+                                    ctypes.byref(mt), ctypes.byref(mk))
+    return st, {"n_superbatches": ns.value, "max_sb_texts": mt.value, "max_sb_tokens": mk.value}
+
+
 def surge_encoder_create(desc: EncoderDesc, weights: Sequence[np.ndarray],
                          max_tokens_per_chunk: int) -> int:
-    arrs = [np.ascontiguousarray(w, dtype=np.float32) for w in weights]
+    """weights: float32 arrays (desc.weight_dtype = F32) or uint16 arrays of
+    bf16 bit patterns (BF16), in the fixed order."""
+    dt = np.float32 if desc.weight_dtype == SURGE_WEIGHTS_F32 else np.uint16
+    arrs = [np.ascontiguousarray(w, dtype=dt) for w in weights]
     ptrs = (ctypes.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
     h = ctypes.c_void_p(0)
     _check(lib().surge_encoder_create(ctypes.byref(desc), ptrs, len(arrs), max_tokens_per_chunk,

@@ -145,7 +145,7 @@ def test_validate_rejects(case):
 
 @pytest.mark.parametrize("field,value", [("d_model", 96), ("n_heads", 5), ("d_ff", 100),
                                          ("n_layers", 0), ("max_positions", 0),
-                                         ("reserved", 1), ("d_model", 2048)])
+                                         ("weight_dtype", 2), ("d_model", 2048)])
 def test_validate_rejects_bad_desc(field, value):
     d = S.make_desc(2, 128, 2, 512, 30522, 64)
     setattr(d, field, value)
@@ -159,3 +159,48 @@ def test_encoder_create_rejects_bad_arguments_without_touching_the_device():
     with pytest.raises(S.SurgeError) as ei:
         S.surge_encoder_create(d, [np.zeros(1, np.float32)] * 3, 1024)
     assert ei.value.status == S.SURGE_ERR_INVALID_ARGUMENT
+
+
+def test_validate_input_beyond_2_31_tokens():
+    """The whole-input check keeps offsets in int64 and caps only each
+    SuperBatch: 2^23 texts of 512 tokens (2^32 tokens in all) in 1,024
+    partitions pass; a plan whose single SuperBatch reaches 2^31 tokens does
+    not.  Only cu_seqlens and part_offsets exist; no token is allocated."""
+    desc = S.make_desc(12, 768, 12, 3072, 30522, 512)
+    n = 1 << 23
+    cu = np.arange(n + 1, dtype=np.int64) * 512
+    assert cu[-1] == 1 << 32
+    offs = np.arange(1025, dtype=np.int64) * (n // 1024)
+    outs = np.full(1024, 4096, dtype=np.uint64)  # never dereferenced
+    st, info = S.surge_validate_input(desc, n, cu, offs, 4096, 20000, S.SURGE_POLICY_SPLIT, outs)
+    assert st == S.SURGE_OK, S.surge_last_error()
+    assert info == {"n_superbatches": 1024, "max_sb_texts": 8192, "max_sb_tokens": 8192 * 512}
+    # one SuperBatch of 2^22 + 1 texts of 512 tokens: 2^31 + 512 tokens
+    m = (1 << 22) + 1
+    st, _ = S.surge_validate_input(desc, m, cu[:m + 1], np.array([0, m], np.int64), 1 << 30, 0,
+                                   S.SURGE_POLICY_SPLIT, outs[:1])
+    assert st == S.SURGE_ERR_INVALID_ARGUMENT
+    assert "2^31" in S.surge_last_error()
+
+
+def test_validate_input_rejects_and_accepts():
+    desc = S.make_desc(2, 128, 2, 512, 30522, 64)
+    cu = np.array([0, 3, 5, 9, 10], np.int64)
+    offs = np.array([0, 2, 2, 4], np.int64)  # partition 1 is empty
+    outs = np.array([4096, 0, 8192], np.uint64)  # an empty partition may have no output
+    ok, info = S.surge_validate_input(desc, 4, cu, offs, 2, 0, S.SURGE_POLICY_SPLIT, outs)
+    assert ok == S.SURGE_OK and info["n_superbatches"] == 2 and info["max_sb_tokens"] == 5
+    bad = [
+        (desc, 4, cu, offs, 2, 0, S.SURGE_POLICY_SPLIT, np.array([4096, 0, 0], np.uint64)),
+        (desc, 4, np.array([0, 3, 3, 9, 10], np.int64), offs, 2, 0, 0, outs),  # empty text
+        (desc, 4, np.array([0, 3, 5, 70, 71], np.int64), offs, 2, 0, 0, outs),  # > max_positions
+        (desc, 4, np.array([1, 3, 5, 9, 10], np.int64), offs, 2, 0, 0, outs),  # cu[0] != 0
+        (desc, 5, np.array([0, 3, 5, 9, 10, 11], np.int64), offs, 2, 0, 0, outs),  # offs end
+        (desc, 4, cu, np.array([0, 3, 2, 4], np.int64), 2, 0, 0, outs),  # decreasing
+        (desc, 4, cu, offs, 0, 0, 0, outs),  # b_min < 1
+        (desc, 4, cu, offs, 2, 0, 7, outs),  # policy
+    ]
+    for args in bad:
+        st, _ = S.surge_validate_input(*args)
+        assert st == S.SURGE_ERR_INVALID_ARGUMENT, args
+        assert S.surge_last_error()

@@ -203,6 +203,11 @@ def test_lemma1_bound(sizes, b_min, cap):
         r2 = max([sb.n_texts for sb in OP.plan(offs, b_min, cap, OP.R2)] + [0])
         assert r1 <= b_min - 1 + n_big
         assert r2 <= cap
+        assert r1 <= OP.largest_superbatch_bound(b_min, n_big, 0, OP.R1)
+        assert r2 <= OP.largest_superbatch_bound(b_min, n_big, cap, OP.R2)
+        # M(S) grows with S, so the bound on S bounds the memory too (Lemma 1)
+        assert OP.superbatch_memory(r2, 47, 384) <= OP.superbatch_memory(
+            OP.largest_superbatch_bound(b_min, n_big, cap, OP.R2), 47, 384)
 
 
 def test_lemma1_table_heavy():
@@ -215,5 +220,18 @@ def test_lemma1_table_heavy():
     assert all(r["max_texts"] <= spec.n_max for r in r2)
     # without the cap a single oversized partition drives the largest call
     assert all(r["max_texts"] > 10 * spec.n_max for r in r1)
-    m = OP.superbatch_memory(10, 100, 384)
-    assert m == 100 * 4 + 4 * 10 * 384
+
+
+def test_lemma1_memory_worked_example(golden_dir):
+    """M(S) = S L + 4 S d against the paper's worked example (Sec. 4.3):
+    500K texts of 47 bytes with d = 384 hold 23.5 MB of text and 768 MB of
+    embeddings, 791.5 MB in all; eq. (memory) rounds it to 791 MB."""
+    g = json.load(open(os.path.join(golden_dir, "lemma1_memory.json")))
+    S, L, d = g["S"], g["L_bytes"], g["d"]
+    total = OP.superbatch_memory(S, L, d)
+    assert total == pytest.approx(g["total_MB"] * 1e6, abs=0.5)
+    assert OP.superbatch_memory(S, L, 0) == pytest.approx(g["text_MB"] * 1e6, abs=0.5)
+    assert OP.superbatch_memory(S, 0, d) == pytest.approx(g["embeddings_MB"] * 1e6, abs=0.5)
+    assert round(total / 1e6) == pytest.approx(g["eq_memory_MB_rounded"], abs=1)
+    # int32 token IDs on the device: L = 4 bytes per token of the text
+    assert OP.device_superbatch_memory(S, 12 * S, d) == OP.superbatch_memory(S, 48, d)

@@ -50,7 +50,7 @@ def _encode_all(torch, enc, wl, d, b_min, n_max, policy=S.SURGE_POLICY_SPLIT):
 
 
 def _oracle_rows(spec, weights, wl, idx):
-    w = E.as_f64(weights)
+    w = E.as_f32(weights)
     sh = spec.encoder
     return E.encode_texts(w, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, idx, sh.ln_eps)
 
@@ -285,3 +285,89 @@ def test_texts_at_the_position_limit(name):
     assert not np.isnan(got).any()
     ref = _oracle_rows(spec, weights, wl, range(wl.n_texts))
     assert_parity(got, ref, name)
+
+
+@pytest.mark.parametrize("name", ["tiny", "bge"])
+def test_bert_style_init_end_to_end(name):
+    """BERT-style initialisation (biases 0, LayerNorm gamma 1, beta 0) end
+    to end, every text against the oracle: the degenerate affine parameters
+    the folded LayerNorm epilogues must also get right."""
+    torch = torch_cuda()
+    spec = W.WORKLOADS[name]
+    sh = spec.encoder
+    base = W.make_workload(spec)
+    n = 160
+    sizes = [40, 0, 1, 79, 40]
+    wl = W.workload_from_lengths(spec, sizes, base.lengths[:n], seed=8)
+    weights = W.make_weights(sh, seed=3, init="bert")
+    assert not weights["layer0.b_qkv"].any() and (weights["layer0.ln1_g"] == 1).all()
+    print(f"[bert init {name}] texts={wl.n_texts} tokens={wl.n_tokens}", flush=True)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    got, _ = _encode_all(torch, enc, wl, sh.d_model, 64, 100)
+    enc.close()
+    assert not np.isnan(got).any()
+    ref = _oracle_rows(spec, weights, wl, range(wl.n_texts))
+    assert_parity(got, ref, name)
+
+
+def test_bf16_host_weights_give_the_same_encoder():
+    """An encoder created from bf16 host arrays (a bf16 checkpoint) and one
+    created from float32 arrays holding the same values produce bit-identical
+    embeddings (bge shapes, whose weights are bf16-valued)."""
+    torch = torch_cuda()
+    import dataclasses
+    spec = dataclasses.replace(W.WORKLOADS["bge"], n_texts=600, n_parts=12)
+    wl = W.make_workload(spec)
+    sh = spec.encoder
+    weights = W.make_weights(sh, seed=spec.seed)
+    f32 = weight_list(sh, weights)
+    bits = []
+    for a in f32:
+        u = np.ascontiguousarray(a, np.float32).view(np.uint32)
+        assert not (u & 0xFFFF).any()  # bf16-representable
+        bits.append((u >> 16).astype(np.uint16))
+    print(f"[bf16 weights] texts={wl.n_texts} tokens={wl.n_tokens}", flush=True)
+    a_enc = S.Encoder(desc_of(sh), f32, 1 << 16)
+    a, _ = _encode_all(torch, a_enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    a_enc.close()
+    desc = desc_of(sh)
+    desc.weight_dtype = S.SURGE_WEIGHTS_BF16
+    b_enc = S.Encoder(desc, bits, 1 << 16)
+    b, _ = _encode_all(torch, b_enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    b_enc.close()
+    assert not np.isnan(a).any()
+    assert np.array_equal(a, b)
+    ref = _oracle_rows(spec, weights, wl, range(0, wl.n_texts, 50))
+    assert_parity(b[::50], ref, "bge")
+
+
+def test_calls_on_two_streams_without_host_sync():
+    """Two encode_all calls of one encoder on two different streams, the
+    second issued while the first may still run: the encoder orders them (its
+    workspace and metadata buffers are shared), so each call's rows equal
+    those of the same call made alone."""
+    torch = torch_cuda()
+    import dataclasses
+    spec = dataclasses.replace(W.WORKLOADS["minilm"], n_texts=20000, n_parts=80)
+    wl = W.make_workload(spec)
+    sh = spec.encoder
+    weights = W.make_weights(sh, seed=spec.seed)
+    enc = S.Encoder(desc_of(sh), weight_list(sh, weights), 1 << 16)
+    print(f"[two streams] texts={wl.n_texts} tokens={wl.n_tokens}", flush=True)
+    ref, _ = _encode_all(torch, enc, wl, sh.d_model, spec.b_min, spec.n_max)
+    tok = torch.from_numpy(wl.tokens).cuda()
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    torch.cuda.synchronize()
+    for k, (s, b_min, n_max) in enumerate([(sa, spec.b_min, spec.n_max), (sb, 700, 900),
+                                           (sa, 2500, 0), (sb, spec.b_min, spec.n_max)]):
+        out, ptrs = _outputs(torch, wl, sh.d_model)
+        enc.encode_all(wl.n_texts, tok, wl.cu_seqlens, wl.part_offsets, b_min, n_max, ptrs,
+                       stream=s)
+        outs.append(out)
+    enc.check(sa)
+    enc.check(sb)
+    torch.cuda.synchronize()
+    enc.close()
+    for k, out in enumerate(outs):
+        assert np.array_equal(out.cpu().numpy(), ref), f"call {k}"

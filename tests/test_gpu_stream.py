@@ -78,13 +78,24 @@ def test_streamed_matches_encode_all(overlap):
         assert np.all(times[:, 2] == 0) and st["d2h_ms"] == 0
     else:
         assert np.all(times[:, 2] > 0)
+    # Lemma 1 (Sec. 4.3): the staging holds two SuperBatches' data-resident
+    # state, M(S) = S L + 4 S d with the text part as int32 token IDs, for the
+    # plan's largest SuperBatch (the embeddings only when they are downloaded)
+    sbs = OP.plan(wl.part_offsets, b_min, n_max, OP.R2)
+    max_txt = max(sb.n_texts for sb in sbs)
+    max_tok = max(int(wl.cu_seqlens[sb.text_end] - wl.cu_seqlens[sb.text_begin]) for sb in sbs)
+    assert (st["max_sb_texts"], st["max_sb_tokens"]) == (max_txt, max_tok)
+    want = 2 * OP.device_superbatch_memory(0 if overlap == 2 else max_txt, max_tok, sh.d_model)
+    assert st["staging_bytes"] == want
+    assert max_txt <= OP.largest_superbatch_bound(b_min, int(np.diff(wl.part_offsets).max()),
+                                                  n_max, OP.R2)
     assert st["enc_ms"] == pytest.approx(times[:, 1].sum(), rel=1e-6)
     if overlap == 0:
         # one stream: the phases add up
         assert st["total_ms"] >= 0.99 * (st["enc_ms"] + st["h2d_ms"] + st["d2h_ms"])
     # a sample against the oracle, so the streamed path is pinned on its own
     idx = [0, 1, wl.n_texts // 2, wl.n_texts - 1]
-    w = E.as_f64(weights)
+    w = E.as_f32(weights)
     oref = E.encode_texts(w, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, idx, sh.ln_eps)
     assert_parity(got[idx], oref, "minilm")
 

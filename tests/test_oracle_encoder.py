@@ -312,3 +312,71 @@ def test_discrimination_record():
     off = c[~np.eye(40, dtype=bool)]
     assert np.median(off) < 0.8
     assert off.max() < 0.99
+
+
+@pytest.mark.parametrize("name,lengths", [
+    ("tiny", [1, 2, 8, 17, 33, 64]),
+    ("minilm", [4, 31, 32, 33, 128]),
+    ("bge", [4, 48, 97, 256]),
+    ("large", [8, 96, 512]),
+])
+def test_float32_oracle_agrees_with_float64_twin(name, lengths):
+    """The float32 oracle (the one the GPU path is held to) against its
+    float64 twin: per-text cosine >= 1 - 1e-9 and max-abs <= 1e-5, i.e. its
+    own rounding is orders of magnitude below the bf16 tolerance."""
+    spec = W.WORKLOADS[name]
+    sh = spec.encoder
+    wl = W.workload_from_lengths(spec, [len(lengths)], lengths, seed=6)
+    w = W.make_weights(sh, seed=spec.seed)
+    w32, w64 = E.as_f32(w), E.as_f64(w)
+    ids = wl.tokens[:lengths[0]]
+    assert E.hidden_states(w32, sh.n_layers, sh.n_heads, ids, sh.ln_eps).dtype == np.float32
+    idx = range(len(lengths))
+    a = E.encode_texts(w32, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, idx, sh.ln_eps)
+    b = E.encode_texts(w64, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, idx, sh.ln_eps)
+    assert a.dtype == np.float32 and b.dtype == np.float64
+    a = a.astype(np.float64)
+    cos = (a * b).sum(1) / (np.linalg.norm(a, axis=1) * np.linalg.norm(b, axis=1))
+    assert cos.min() >= 1.0 - 1e-9
+    assert np.max(np.abs(a - b)) <= 1e-5
+
+
+def test_centred_bounds_record(golden_dir):
+    """The supplementary centred-cosine bounds of the GPU tests: derived from
+    a bf16 simulation of the oracle for every configuration, all tighter than
+    the acceptance cosine yet looser than what the simulation reached, and
+    still rejecting a planted cross-text attention leak."""
+    rec = json.load(open(os.path.join(golden_dir, "centred_bounds.json")))
+    assert set(rec["configs"]) == set(W.WORKLOADS)
+    for name, r in rec["shapes"].items():
+        assert r["n_texts"] >= 100
+        assert 0.995 < r["bound"] < r["sim_centred_min"] < 1.0
+        assert r["sim_cos_min"] >= 0.9995 and r["sim_maxabs"] <= 2e-2
+        if "leak_centred_min" in r:
+            assert r["leak_centred_min"] < r["bound"]
+
+
+def test_centred_bound_holds_for_a_fresh_bf16_simulation(golden_dir):
+    """Re-run the bound's bf16 simulation on texts it was not derived from
+    (tiny encoder, texts 200-215): they stay above the recorded bound."""
+    import importlib.util
+    spec_ = importlib.util.spec_from_file_location(
+        "derive_centred_bounds", os.path.join(golden_dir, "derive_centred_bounds.py"))
+    D = importlib.util.module_from_spec(spec_)
+    spec_.loader.exec_module(D)
+    rec = json.load(open(os.path.join(golden_dir, "centred_bounds.json")))
+    spec = W.WORKLOADS["tiny"]
+    sh = spec.encoder
+    wl = W.make_workload(spec)
+    w32 = E.as_f32(W.make_weights(sh, seed=spec.seed))
+    wb = {k: D.bf16(v) for k, v in w32.items()}
+    idx = list(range(200, 216))
+    ref = E.encode_texts(w32, sh.n_layers, sh.n_heads, wl.tokens, wl.cu_seqlens, idx, sh.ln_eps)
+    sim = np.stack([E.mean_pool_l2(D.hidden_bf16(wb, sh.n_layers, sh.n_heads,
+                                                 wl.tokens[wl.cu_seqlens[i]:wl.cu_seqlens[i + 1]],
+                                                 sh.ln_eps)) for i in idx])
+    assert D.centred_min(sim, ref) >= rec["configs"]["tiny"]
+    # bf16() is round-to-nearest-even: 1 + 2^-8 is a tie between 1 and
+    # 1 + 2^-7 and goes to the even one (1); 1 + 3 * 2^-8 goes up
+    assert D.bf16(np.float32([1 + 2 ** -8, 1 + 3 * 2 ** -8, -2.5]))[0] == 1.0
+    assert D.bf16(np.float32([1 + 3 * 2 ** -8]))[0] == np.float32(1 + 2 ** -6)
