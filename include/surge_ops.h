@@ -71,6 +71,28 @@ surge_status surge_op_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t*
                                 const float* d_col_s, const float* d_gamma, const float* d_beta,
                                 float eps, float* d_stats_out, uint16_t* d_y, void* hip_stream);
 
+/*
+ * surge_op_linear_ln without any allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the per-row LayerNorm factors that the
+ * folded and residual-LayerNorm epilogues (3, 4, 6) read live in a static
+ * device array of the library (4 MiB: at most 524,288 rows), not in a buffer
+ * allocated per call.  Same arguments, checks, kernels and results as
+ * surge_op_linear_ln, but asynchronous: the call only enqueues on
+ * `hip_stream` (no synchronisation).  M above 524,288 with epilogue 3, 4 or
+ * 6 returns SURGE_ERR_CAPACITY before anything is enqueued.  Every call on
+ * one GPU shares that GPU's array (each call overwrites the rows it uses
+ * before reading them): calls on one stream are ordered, calls that overlap
+ * on different streams of one GPU race.  Calls no hipMalloc/hipFree.
+ */
+surge_status surge_op_linear_ln_noalloc(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                                        const uint16_t* d_w, const float* d_bias,
+                                        const uint16_t* d_res, int32_t epilogue,
+                                        const float* d_stats_in, int32_t parts_in,
+                                        const float* d_col_s, const float* d_gamma,
+                                        const float* d_beta, float eps, float* d_stats_out,
+                                        uint16_t* d_y, void* hip_stream);
+
 /* Features per statistics partial of an [M, N] linear output (host-only). */
 int32_t surge_op_linear_stats_width(int64_t M, int32_t N);
 

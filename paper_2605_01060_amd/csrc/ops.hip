@@ -1,6 +1,7 @@
 // Stage-level entry points: one kernel of the encode path on caller buffers.
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "internal.h"
@@ -48,6 +49,36 @@ surge_status upload_cu(int64_t n_texts, const int64_t* cu, int64_t max_len, Devi
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Scratch of surge_op_linear_ln_noalloc: the per-row LayerNorm factors of at
+// most kScratchRows rows (4 MiB), held by every GPU the library runs on until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: host code uses only the per-device address obtained from
+// hipGetSymbolAddress below.
+constexpr int64_t kScratchRows = 1 << 19;
+static __device__ __align__(256) float2 scratch[kScratchRows];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+float2* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of the current device's scratch, looked up once per
+// device with that device current.
+surge_status scratch_address(float2** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SURGE_ERR_DEVICE, "device index %d outside [0, %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SURGE_ERR_DEVICE, "hipGetSymbolAddress returned NULL");
+    g_scratch_ptr[dev] = (float2*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SURGE_OK;
+}
 
 }  // namespace
 
@@ -103,12 +134,17 @@ surge_status surge_op_linear(int64_t M, int32_t N, int32_t K, const uint16_t* d_
   return SURGE_OK;
 }
 
-surge_status surge_op_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
-                                const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
-                                int32_t epilogue, const float* d_stats_in, int32_t parts_in,
-                                const float* d_col_s, const float* d_gamma, const float* d_beta,
-                                float eps, float* d_stats_out, uint16_t* d_y, void* hip_stream) {
-  clear_error();
+}  // extern "C"
+
+namespace {
+
+// Argument check shared by surge_op_linear_ln and its no-allocation variant;
+// *rows is set when the epilogue reads per-row LayerNorm factors.
+surge_status check_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                             const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
+                             int32_t epilogue, const float* d_stats_in, int32_t parts_in,
+                             const float* d_col_s, const float* d_gamma, const float* d_beta,
+                             float eps, float* d_stats_out, uint16_t* d_y, bool* rows) {
   if (M < 1 || M > (int64_t)INT32_MAX) return fail(SURGE_ERR_INVALID_ARGUMENT, "M=%lld", (long long)M);
   if (N < 128 || N % 128) return fail(SURGE_ERR_INVALID_ARGUMENT, "N=%d not a multiple of 128", N);
   if (K < 64 || K % 64) return fail(SURGE_ERR_INVALID_ARGUMENT, "K=%d not a multiple of 64", K);
@@ -131,21 +167,79 @@ surge_status surge_op_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t*
       (d_gamma && !aligned16(d_gamma)) || (d_beta && !aligned16(d_beta)) ||
       (d_stats_in && ((uintptr_t)d_stats_in & 7u)) || (d_stats_out && ((uintptr_t)d_stats_out & 7u)))
     return fail(SURGE_ERR_INVALID_ARGUMENT, "device buffers must be aligned (16 B; stats 8 B)");
+  *rows = fold || lnres;
+  return SURGE_OK;
+}
+
+// Enqueue the row factors (when `rows` is not NULL) and the linear layer.
+surge_status enqueue_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                               const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
+                               int32_t epilogue, const float* d_stats_in, int32_t parts_in,
+                               const float* d_col_s, const float* d_gamma, const float* d_beta,
+                               float eps, float* d_stats_out, uint16_t* d_y, float2* rows,
+                               hipStream_t s) {
   LinearExtra ex;
   ex.stats_out = (float2*)d_stats_out;
   ex.col_s = d_col_s;
   ex.gamma = d_gamma;
   ex.beta = d_beta;
-  hipStream_t s = (hipStream_t)hip_stream;
-  DeviceCu rows;  // per-row LayerNorm factors, freed on return
-  if (fold || lnres) {
-    HIP_TRY(hipMalloc(&rows.ptr, (size_t)M * 8));
-    HIP_TRY(launch_ln_rows((const float2*)d_stats_in, parts_in, M, eps, (float2*)rows.ptr, s));
-    ex.rows_in = (const float2*)rows.ptr;
+  if (rows) {
+    HIP_TRY(launch_ln_rows((const float2*)d_stats_in, parts_in, M, eps, rows, s));
+    ex.rows_in = rows;
   }
   HIP_TRY(launch_linear(d_x, d_w, d_bias, d_res, d_y, M, N, K, epilogue, ex, s));
+  return SURGE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+surge_status surge_op_linear_ln(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                                const uint16_t* d_w, const float* d_bias, const uint16_t* d_res,
+                                int32_t epilogue, const float* d_stats_in, int32_t parts_in,
+                                const float* d_col_s, const float* d_gamma, const float* d_beta,
+                                float eps, float* d_stats_out, uint16_t* d_y, void* hip_stream) {
+  clear_error();
+  bool need_rows = false;
+  surge_status st = check_linear_ln(M, N, K, d_x, d_w, d_bias, d_res, epilogue, d_stats_in,
+                                    parts_in, d_col_s, d_gamma, d_beta, eps, d_stats_out, d_y,
+                                    &need_rows);
+  if (st != SURGE_OK) return st;
+  hipStream_t s = (hipStream_t)hip_stream;
+  DeviceCu rows;  // per-row LayerNorm factors, freed on return
+  if (need_rows) HIP_TRY(hipMalloc(&rows.ptr, (size_t)M * 8));
+  st = enqueue_linear_ln(M, N, K, d_x, d_w, d_bias, d_res, epilogue, d_stats_in, parts_in, d_col_s,
+                         d_gamma, d_beta, eps, d_stats_out, d_y, (float2*)rows.ptr, s);
+  if (st != SURGE_OK) return st;
   HIP_TRY(hipStreamSynchronize(s));
   return SURGE_OK;
+}
+
+surge_status surge_op_linear_ln_noalloc(int64_t M, int32_t N, int32_t K, const uint16_t* d_x,
+                                        const uint16_t* d_w, const float* d_bias,
+                                        const uint16_t* d_res, int32_t epilogue,
+                                        const float* d_stats_in, int32_t parts_in,
+                                        const float* d_col_s, const float* d_gamma,
+                                        const float* d_beta, float eps, float* d_stats_out,
+                                        uint16_t* d_y, void* hip_stream) {
+  clear_error();
+  bool need_rows = false;
+  surge_status st = check_linear_ln(M, N, K, d_x, d_w, d_bias, d_res, epilogue, d_stats_in,
+                                    parts_in, d_col_s, d_gamma, d_beta, eps, d_stats_out, d_y,
+                                    &need_rows);
+  if (st != SURGE_OK) return st;
+  float2* rows = nullptr;
+  if (need_rows) {
+    if (M > kScratchRows)
+      return fail(SURGE_ERR_CAPACITY, "M=%lld rows exceed the %lld rows of the static scratch",
+                  (long long)M, (long long)kScratchRows);
+    st = scratch_address(&rows);
+    if (st != SURGE_OK) return st;
+  }
+  return enqueue_linear_ln(M, N, K, d_x, d_w, d_bias, d_res, epilogue, d_stats_in, parts_in,
+                           d_col_s, d_gamma, d_beta, eps, d_stats_out, d_y, rows,
+                           (hipStream_t)hip_stream);
 }
 
 int32_t surge_op_linear_stats_width(int64_t M, int32_t N) { return linear_stats_width(M, N); }

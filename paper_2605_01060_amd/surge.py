@@ -92,6 +92,8 @@ _SIGNATURES = {
     "surge_op_linear": ([_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P], _I32),
     "surge_op_linear_ln": ([_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P, _P, _P,
                             ctypes.c_float, _P, _P, _P], _I32),
+    "surge_op_linear_ln_noalloc": ([_I64, _I32, _I32, _P, _P, _P, _P, _I32, _P, _I32, _P, _P,
+                                    _P, ctypes.c_float, _P, _P, _P], _I32),
     "surge_op_linear_stats_width": ([_I64, _I32], _I32),
     "surge_op_attention": ([_I64, _P, _I32, _I32, _P, _P, _P], _I32),
     "surge_op_layernorm": ([_I64, _I32, _P, _P, _P, ctypes.c_float, _P, _P], _I32),
@@ -335,6 +337,16 @@ def surge_op_linear_ln(M, N, K, x, w, bias, res, epilogue, stats_in, parts_in, c
     _check(lib().surge_op_linear_ln(M, N, K, _dev(x), _dev(w), _dev(bias), _dev(res), epilogue,
                                     _dev(stats_in), parts_in, _dev(col_s), _dev(gamma),
                                     _dev(beta), eps, _dev(stats_out), _dev(y), _stream(stream)))
+
+
+def surge_op_linear_ln_noalloc(M, N, K, x, w, bias, res, epilogue, stats_in, parts_in, col_s,
+                               gamma, beta, eps, stats_out, y, stream=None):
+    """As surge_op_linear_ln, with the row factors in the library's static
+    scratch; only enqueues on `stream`."""
+    _check(lib().surge_op_linear_ln_noalloc(M, N, K, _dev(x), _dev(w), _dev(bias), _dev(res),
+                                            epilogue, _dev(stats_in), parts_in, _dev(col_s),
+                                            _dev(gamma), _dev(beta), eps, _dev(stats_out), _dev(y),
+                                            _stream(stream)))
 
 
 def surge_op_linear_stats_width(M: int, N: int) -> int:
