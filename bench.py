@@ -295,9 +295,10 @@ def main(argv=None):
                         "avg_launch_ms": s["total_ms"] / s["launches"]}
 
     # Streamed pass, outside the timed region: tokens start in pinned host
-    # memory and embeddings end there, so PCIe is included; once with the
-    # copies overlapped on a second stream, once on one stream in order, and
-    # once zero-copy (the pooling kernel writes the pinned output directly).
+    # memory and embeddings end there, so PCIe is included.  The reported
+    # rate is the zero-copy mode (the pooling kernel writes the pinned output
+    # directly, so no download runs); beside it the copies overlapped on a
+    # second stream and everything in order on one stream.
     streamed = None
     if not args.no_stream:
         h_tok = torch.from_numpy(wl.tokens).pin_memory()
@@ -315,15 +316,21 @@ def main(argv=None):
                                       compute_stream=cs)
         enc_sb = times[:, 1]
         streamed = {
-            "value": wl.n_texts / (st1["total_ms"] / 1e3), "unit": "texts/s",
-            "total_ms": st1["total_ms"], "ttfo_ms": st1["ttfo_ms"], "enc_ms": st1["enc_ms"],
-            "h2d_ms": st1["h2d_ms"], "d2h_ms": st1["d2h_ms"], "rho": st1["rho"],
-            "rho_measured": st1["rho_measured"],
+            "value": wl.n_texts / (st2["total_ms"] / 1e3), "unit": "texts/s",
+            "mode": "zero copy (overlap=2): tokens uploaded in order, embeddings written "
+                    "into pinned host memory by the pooling kernel",
+            "total_ms": st2["total_ms"], "ttfo_ms": st2["ttfo_ms"], "enc_ms": st2["enc_ms"],
+            "h2d_ms": st2["h2d_ms"],
+            "staging_bytes": st2["staging_bytes"], "max_sb_texts": st2["max_sb_texts"],
+            "max_sb_tokens": st2["max_sb_tokens"],
+            "overlapped_value": wl.n_texts / (st1["total_ms"] / 1e3),
+            "overlapped_total_ms": st1["total_ms"], "overlapped_ttfo_ms": st1["ttfo_ms"],
+            "overlapped_h2d_ms": st1["h2d_ms"], "overlapped_d2h_ms": st1["d2h_ms"],
+            "overlapped_rho": st1["rho"], "overlapped_rho_measured": st1["rho_measured"],
+            "overlapped_staging_bytes": st1["staging_bytes"],
             "sync_value": wl.n_texts / (st0["total_ms"] / 1e3),
             "sync_total_ms": st0["total_ms"], "sync_ttfo_ms": st0["ttfo_ms"],
             "sync_rho_measured": st0["rho_measured"],
-            "zero_copy_value": wl.n_texts / (st2["total_ms"] / 1e3),
-            "zero_copy_total_ms": st2["total_ms"], "zero_copy_ttfo_ms": st2["ttfo_ms"],
             "superbatch_encode_ms": {"n": int(enc_sb.size), "min": float(enc_sb.min()),
                                      "median": float(np.median(enc_sb)),
                                      "max": float(enc_sb.max())},

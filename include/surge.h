@@ -269,7 +269,10 @@ typedef struct surge_stream_stats {
  * device mapping, so no download runs at all; h_out must then be pinned
  * host memory mapped for the device (hipHostMalloc) over all n_texts rows,
  * else SURGE_ERR_INVALID_ARGUMENT before anything runs, and the download
- * times read 0.  Returns after both streams have finished.
+ * times read 0.  Returns after both streams have finished.  Zero copy is
+ * the fastest of the three on MI355X: the runtime moves pinned-memory
+ * copies with copy kernels that take compute units from the encode, so the
+ * double-buffered overlap gains nothing over the in-order mode.
  *
  * h_token_ids: host int32 [h_cu_seqlens[n_texts]], texts back to back.
  * h_cu_seqlens: host int64 [n_texts+1], global.  h_part_offsets: host int64

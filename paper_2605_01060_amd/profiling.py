@@ -8,6 +8,8 @@
 `mfma` turns a `--pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES` run into
 the MFMA-busy share of each kernel class (MFMA busy cycles summed over the
 SIMDs / (4 SIMDs x CU busy cycles)).
+`clock` turns a `--pmc GRBM_GUI_ACTIVE` run into the engine clock of each
+kernel class.
 `traffic` reads two `--pmc` runs (FETCH_SIZE, then WRITE_SIZE, KiB per
 dispatch), scales each by what the same counter reads for the plain device
 copy of known size that the benchmark runs first (`--copy-calibration-mb`),
@@ -139,6 +141,31 @@ def mfma_busy(csv_path: str) -> Dict[str, Dict[str, float]]:
                 "dispatches": v["dispatches"]} for k, v in per.items()}
 
 
+def clock(csv_path: str, nominal_ghz: float = 2.4, peak_tflops: float = 2516.6
+          ) -> Dict[str, Dict[str, float]]:
+    """Mean engine clock of each kernel class from a `--pmc GRBM_GUI_ACTIVE`
+    run: the counter is summed over the 8 XCDs, so the clock of a dispatch
+    is GRBM_GUI_ACTIVE / 8 / duration.  Also the bf16 MFMA peak at that
+    clock (the nominal peak scaled by clock / 2.4 GHz)."""
+    per: Dict[str, Dict[str, float]] = {}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != "GRBM_GUI_ACTIVE":
+            continue
+        dur = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+        for cls, (_, pred) in KERNEL_CLASSES.items():
+            if pred(r["Kernel_Name"]) and dur > 0:
+                e = per.setdefault(cls, {"cycles": 0.0, "ns": 0.0, "dispatches": 0})
+                e["cycles"] += float(r["Counter_Value"]) / 8.0
+                e["ns"] += dur
+                e["dispatches"] += 1
+    out = {}
+    for k, v in per.items():
+        ghz = v["cycles"] / v["ns"]
+        out[k] = {"dispatches": v["dispatches"], "mean_us": v["ns"] / v["dispatches"] / 1e3,
+                  "ghz": ghz, "peak_at_clock_tflops": peak_tflops * ghz / nominal_ghz}
+    return out
+
+
 # bench.py kernel names -> traffic class under profiles/
 BENCH_TRAFFIC = {"qkv": "qkv", "ffn1": "ffn1", "oproj": "residual", "ffn2": "residual",
                  "attn": "attn", "ln1": "layernorm", "ln2": "layernorm"}
@@ -147,9 +174,11 @@ MFMA_CLASSES = ("qkv", "oproj", "ffn1", "ffn2")
 
 def roofline_markdown(bench_json: str, workload: str, command: str,
                       peak_tflops: float = 2516.6, peak_gbs: float = 8000.0) -> str:
-    """Every kernel class of one benchmark line against its roof: MFMA
-    classes by algorithmic TFLOP/s, the others by algorithmic GB/s, with the
-    measured HBM bytes per launch where profiles/ holds a current figure."""
+    """Every kernel class of one benchmark line against its own roof: the
+    time it would take at the bf16 MFMA peak on its algorithmic FLOPs and at
+    the HBM peak on its algorithmic bytes, whichever is longer (the bound),
+    with the fraction of that roof achieved, and the measured HBM bytes per
+    launch where profiles/ holds a current figure."""
     d = json.load(open(bench_json))
     if d.get("kernels_from"):
         # per-kernel times from one untimed profiled step; the roofline
@@ -157,9 +186,10 @@ def roofline_markdown(bench_json: str, workload: str, command: str,
         src, steps = d["kernels_from"], 1
     else:
         src, steps = "HIP events inside the timed region", d["steps"]
+    ridge = peak_tflops * 1e12 / (peak_gbs * 1e9)
     lines = [f"From `{command}` (one JSON line; per-kernel times: {src}) and the traffic "
              f"summaries under `profiles/`.", "",
-             f"Value: {d['value']:.0f} texts/s, {d['ms_per_step']:.0f} ms per step, "
+             f"Value: {d['value']:.0f} texts/s, {d['ms_per_step']:.1f} ms per step, "
              f"MFMA util {d['mfma_util_pct']:.1f} % of {peak_tflops} TFLOP/s."]
     rf = d.get("roofline")
     if rf:
@@ -167,23 +197,37 @@ def roofline_markdown(bench_json: str, workload: str, command: str,
                      f"{rf['achieved']:.0f} {rf['unit']} of {rf['peak']} "
                      f"(frac {rf['frac']:.3f}), {rf['avg_launch_ms']:.3f} ms per launch.")
     lines += ["",
-              "| kernel | launches/step | ms/step | achieved | roof | % of roof | "
-              "HBM bytes/launch (measured) | algorithmic bytes/launch |",
-              "|---|---|---|---|---|---|---|---|"]
+              f"Roofs: bf16 MFMA {peak_tflops} TFLOP/s, HBM {peak_gbs:.0f} GB/s (ridge "
+              f"{ridge:.0f} FLOP/B).  A kernel's roof time is the longer of its algorithmic "
+              "FLOPs at the MFMA peak and its algorithmic bytes at the HBM peak.", "",
+              "| kernel | launches/step | ms/step | TFLOP/s | GB/s (algorithmic) | FLOP/B | "
+              "bound | roof ms/step | % of roof | HBM bytes/launch (measured) | "
+              "algorithmic bytes/launch |",
+              "|---|---|---|---|---|---|---|---|---|---|---|"]
+    tot_ms = tot_roof = 0.0
     for k, v in d["kernels"].items():
         per_launch_bytes = None
         if k in BENCH_TRAFFIC:
             per_launch_bytes = load_traffic(BENCH_TRAFFIC[k], workload)
-        alg_bytes = v["gbs"] * 1e9 * v["avg_ms"] / 1e3 if "gbs" in v else None
-        if k in MFMA_CLASSES and "tflops" in v:
-            ach, roof, unit = v["tflops"], peak_tflops, "TFLOP/s"
-        else:
-            ach, roof, unit = v.get("gbs", 0.0), peak_gbs, "GB/s"
+        ms = v["total_ms_per_step"]
+        flops = v.get("tflops", 0.0) * 1e12 * ms / 1e3
+        nbytes = v.get("gbs", 0.0) * 1e9 * ms / 1e3
+        t_mfma = flops / (peak_tflops * 1e12) * 1e3
+        t_hbm = nbytes / (peak_gbs * 1e9) * 1e3
+        roof = max(t_mfma, t_hbm)
+        bound = "mfma" if t_mfma >= t_hbm else "hbm"
+        ai = flops / nbytes if nbytes else float("inf")
+        tot_ms += ms
+        tot_roof += roof
+        alg_bytes = nbytes / v["launches"] * steps if nbytes else None
         lines.append(
-            f"| {k} | {v['launches'] / steps:.0f} | {v['total_ms_per_step']:.1f} | "
-            f"{ach:.0f} {unit} | {roof:.0f} {unit} | {100 * ach / roof:.1f} | "
+            f"| {k} | {v['launches'] / steps:.0f} | {ms:.1f} | {v.get('tflops', 0.0):.0f} | "
+            f"{v.get('gbs', 0.0):.0f} | {ai:.0f} | {bound} | {roof:.1f} | "
+            f"{100 * roof / ms if ms else 0.0:.1f} | "
             f"{'%.3g' % per_launch_bytes if per_launch_bytes else '—'} | "
             f"{'%.3g' % alg_bytes if alg_bytes else '—'} |")
+    lines += ["", f"Sum over kernels: {tot_ms:.1f} ms per step against {tot_roof:.1f} ms of "
+                  f"roof time ({100 * tot_roof / tot_ms:.1f} % of roof)."]
     return "\n".join(lines) + "\n"
 
 
@@ -200,6 +244,9 @@ def main(argv=None):
     c = sub.add_parser("mfma")
     c.add_argument("csv")
     c.add_argument("--command", required=True)
+    k = sub.add_parser("clock")
+    k.add_argument("csv")
+    k.add_argument("--command", required=True)
     b = sub.add_parser("traffic")
     b.add_argument("fetch_csv")
     b.add_argument("write_csv")
@@ -220,6 +267,24 @@ def main(argv=None):
                  "| kernel class | dispatches | MFMA busy % |", "|---|---|---|"]
         for k in sorted(res):
             lines.append(f"| {k} | {res[k]['dispatches']} | {res[k]['mfma_busy_pct']:.1f} |")
+        sys.stdout.write("\n".join(lines) + "\n")
+    elif args.cmd == "clock":
+        res = clock(args.csv)
+        lines = [f"Command: `{args.command}`", "",
+                 "Engine clock per kernel class = GRBM_GUI_ACTIVE (summed over the 8 XCDs) "
+                 "/ 8 / dispatch duration, averaged over the dispatches; the bf16 MFMA peak "
+                 "at that clock is 2516.6 TFLOP/s x clock / 2.4 GHz.", "",
+                 "| kernel class | dispatches | mean duration us | clock GHz | "
+                 "bf16 peak at that clock TFLOP/s |", "|---|---|---|---|---|"]
+        for k in sorted(res):
+            r = res[k]
+            if r["mean_us"] < 50.0:  # counter read-out dominates a short dispatch
+                lines.append(f"| {k} | {r['dispatches']} | {r['mean_us']:.1f} | — | — |")
+            else:
+                lines.append(f"| {k} | {r['dispatches']} | {r['mean_us']:.1f} | "
+                             f"{r['ghz']:.3f} | {r['peak_at_clock_tflops']:.0f} |")
+        lines += ["", "(Dispatches shorter than 50 us: the counter read-out around the "
+                      "dispatch dominates, so no clock is given.)"]
         sys.stdout.write("\n".join(lines) + "\n")
     else:
         rec = traffic(args.fetch_csv, args.write_csv, args.kernel_class, args.copy_mib)

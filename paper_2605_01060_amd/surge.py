@@ -397,7 +397,7 @@ class Encoder:
                                 n_max, policy, part_out_ptrs, first_sb, stream)
 
     def encode_all_streamed(self, n_texts, h_tokens, cu_seqlens, part_offsets, b_min, n_max,
-                            h_out, overlap=1, compute_stream=None, copy_stream=None,
+                            h_out, overlap=2, compute_stream=None, copy_stream=None,
                             policy=SURGE_POLICY_SPLIT, sb_times=None) -> Dict[str, float]:
         return surge_encode_all_streamed(self.handle, n_texts, h_tokens, cu_seqlens, part_offsets,
                                          b_min, n_max, policy, h_out, overlap, compute_stream,

@@ -118,3 +118,40 @@ def test_bench_refuses_more_than_one_gpu(capsys):
     assert bench.main(["--gpus", "2"]) == 2
     out = json.loads(capsys.readouterr().out.strip().splitlines()[-1])
     assert "one GPU" in out["error"]
+
+
+def test_clock_per_kernel_class(tmp_path):
+    """GRBM_GUI_ACTIVE is summed over the 8 XCDs: clock = value / 8 /
+    duration; the MFMA peak scales with it."""
+    path = tmp_path / "clock.csv"
+    ffn1 = LIN.format(epi=4, order=1)
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value",
+                    "Start_Timestamp", "End_Timestamp"])
+        w.writerow([0, ffn1, "GRBM_GUI_ACTIVE", 8 * 2.0 * 1000.0, 5000, 6000])  # 2.0 GHz, 1 us
+        w.writerow([1, ffn1, "GRBM_GUI_ACTIVE", 8 * 2.2 * 3000.0, 7000, 10000])  # 2.2 GHz, 3 us
+        w.writerow([1, ffn1, "SQ_BUSY_CYCLES", 123.0, 7000, 10000])  # other counters ignored
+    res = P.clock(str(path))
+    assert res["ffn1"]["dispatches"] == 2
+    assert res["ffn1"]["ghz"] == pytest.approx((2.0 * 1000 + 2.2 * 3000) / 4000)
+    assert res["ffn1"]["peak_at_clock_tflops"] == pytest.approx(2516.6 * res["ffn1"]["ghz"] / 2.4)
+    assert res["ffn1"]["mean_us"] == pytest.approx(2.0)
+
+
+def test_roofline_bound_follows_arithmetic_intensity(tmp_path, monkeypatch):
+    """A kernel below the ridge (315 FLOP/B) is held to the HBM roof, one
+    above it to the MFMA roof."""
+    monkeypatch.setattr(P, "ROOT", str(tmp_path))
+    line = {"value": 1.0, "ms_per_step": 100.0, "mfma_util_pct": 20.0, "steps": 1,
+            "kernels": {"oproj": {"launches": 10, "total_ms_per_step": 10.0, "avg_ms": 1.0,
+                                  "tflops": 500.0, "gbs": 4000.0},  # 125 FLOP/B
+                        "ffn2": {"launches": 10, "total_ms_per_step": 20.0, "avg_ms": 2.0,
+                                 "tflops": 1000.0, "gbs": 2000.0}}}  # 500 FLOP/B
+    path = tmp_path / "bench.json"
+    path.write_text(json.dumps(line))
+    md = P.roofline_markdown(str(path), "minilm", "python bench.py --workload minilm")
+    oproj = [l for l in md.splitlines() if l.startswith("| oproj ")][0].split("|")
+    ffn2 = [l for l in md.splitlines() if l.startswith("| ffn2 ")][0].split("|")
+    assert oproj[7].strip() == "hbm" and oproj[9].strip() == f"{100 * 4000 / 8000:.1f}"
+    assert ffn2[7].strip() == "mfma" and ffn2[9].strip() == f"{100 * 1000 / 2516.6:.1f}"
