@@ -272,13 +272,11 @@ def main(argv=None):
             ent["gbs"] = s["bytes"] / (s["total_ms"] / 1e3) / 1e9
         kernels[name] = ent
     roofline = None
-    traffic_class = {"qkv": "qkv", "ffn1": "ffn1", "oproj": "residual", "ffn2": "residual",
-                     "attn": "attn", "ln1": "layernorm", "ln2": "layernorm"}
     if dom is not None and kstats[dom]["launches"] > 0:
         s = kstats[dom]
         traffic = None
-        if dom in traffic_class:
-            traffic = profiling.load_traffic(traffic_class[dom], args.workload)
+        if dom in profiling.BENCH_TRAFFIC:
+            traffic = profiling.load_traffic(profiling.BENCH_TRAFFIC[dom], args.workload)
         if dom in MFMA_KERNELS:
             achieved = s["flops"] / (s["total_ms"] / 1e3) / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,

@@ -10,6 +10,8 @@ the MFMA-busy share of each kernel class (MFMA busy cycles summed over the
 SIMDs / (4 SIMDs x CU busy cycles)).
 `clock` turns a `--pmc GRBM_GUI_ACTIVE` run into the engine clock of each
 kernel class.
+`fabric` turns a `--pmc` run of the L2 read-request counters split by
+request size into exact L2-to-fabric read bytes per launch of each class.
 `traffic` reads two `--pmc` runs (FETCH_SIZE, then WRITE_SIZE, KiB per
 dispatch), scales each by what the same counter reads for the plain device
 copy of known size that the benchmark runs first (`--copy-calibration-mb`),
@@ -31,16 +33,10 @@ from typing import Dict, List, Optional, Tuple
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 
-# kernel class -> (source file, predicate on the demangled kernel name)
-# (linear epilogues: 0 bias, 1 bias+GELU, 2 residual, 3 folded LN, 4 folded
-# LN + GELU, 5 residual + row statistics, 6 residual LN + row statistics)
-KERNEL_CLASSES = {
-    "qkv": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) in (0, 3)),
-    "ffn1": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) in (1, 4)),
-    "residual": ("linear.hip", lambda n: "linear_bf16_kernel" in n and _epi(n) in (2, 5, 6)),
-    "attn": ("attention.hip", lambda n: "attention_varlen_kernel" in n),
-    "layernorm": ("rows.hip", lambda n: "layernorm_kernel" in n or "ln_rows_kernel" in n),
-}
+# kernel class -> source file of its kernel
+KERNEL_SOURCES = {"qkv": "linear.hip", "oproj": "linear.hip", "ffn1": "linear.hip",
+                  "ffn2": "linear.hip", "attn": "attention.hip", "layernorm": "rows.hip"}
+KERNEL_CLASSES = tuple(KERNEL_SOURCES)
 COPY_KERNEL = "copyBuffer"
 
 
@@ -51,8 +47,58 @@ def _epi(name: str) -> int:
     return int(m.group(1).split(",")[-2]) if m else -1
 
 
+def name_class(name: str) -> Optional[str]:
+    """Kernel class from the demangled name alone (linear epilogues: 0 bias,
+    1 bias+GELU, 2 residual, 3 folded LN, 4 folded LN + GELU, 5 residual +
+    row statistics, 6 residual LN + row statistics).  The O-projection and
+    FFN2 run the same residual-epilogue instance and come back as
+    "residual"; `dispatch_classes` tells them apart."""
+    if "linear_bf16_kernel" in name:
+        return {0: "qkv", 3: "qkv", 1: "ffn1", 4: "ffn1",
+                2: "residual", 5: "residual", 6: "residual"}.get(_epi(name))
+    if "attention_varlen_kernel" in name:
+        return "attn"
+    if "layernorm_kernel" in name or "ln_rows_kernel" in name:
+        return "layernorm"
+    return None
+
+
+def dispatch_classes(names: List[str]) -> List[Optional[str]]:
+    """Kernel class of every dispatch, given the names in dispatch order: a
+    residual-epilogue GEMM is FFN2 when the linear dispatch before it was
+    FFN1 (the FFN output), and the O-projection otherwise."""
+    out: List[Optional[str]] = []
+    last_linear = None
+    for n in names:
+        c = name_class(n)
+        if c == "residual":
+            c = "ffn2" if last_linear == "ffn1" else "oproj"
+        if c in ("qkv", "ffn1", "oproj", "ffn2"):
+            last_linear = c
+        out.append(c)
+    return out
+
+
+def _dispatches(path: str) -> List[Dict]:
+    """The dispatches of a counter-collection CSV in dispatch order, each
+    with its name, class, duration (ns, where timestamps are present) and
+    counters."""
+    by_id: Dict[int, Dict] = {}
+    for r in csv.DictReader(open(path)):
+        key = int(r.get("Dispatch_Id") or r.get("Correlation_Id"))
+        e = by_id.setdefault(key, {"name": r["Kernel_Name"], "counters": {}, "ns": 0.0})
+        e["counters"][r["Counter_Name"]] = (e["counters"].get(r["Counter_Name"], 0.0)
+                                            + float(r["Counter_Value"]))
+        if r.get("Start_Timestamp") and r.get("End_Timestamp"):
+            e["ns"] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    disp = [by_id[k] for k in sorted(by_id)]
+    for e, c in zip(disp, dispatch_classes([e["name"] for e in disp])):
+        e["cls"] = c
+    return disp
+
+
 def source_hash(kernel_class: str) -> str:
-    fname = KERNEL_CLASSES[kernel_class][0]
+    fname = KERNEL_SOURCES[kernel_class]
     h = hashlib.sha256()
     for f in (fname, "device_common.h"):
         with open(os.path.join(PKG, "csrc", f), "rb") as fh:
@@ -73,28 +119,18 @@ def stats_markdown(path: str, command: str, top: int = 12) -> str:
     return "\n".join(out) + "\n"
 
 
-def _per_dispatch(path: str, counter: str) -> Dict[str, List[float]]:
-    vals: Dict[str, List[float]] = {}
-    for r in csv.DictReader(open(path)):
-        if r["Counter_Name"] != counter:
-            continue
-        vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
-    return vals
-
-
 def traffic(fetch_csv: str, write_csv: str, kernel_class: str, copy_mib: float) -> Dict:
-    pred = KERNEL_CLASSES[kernel_class][1]
     res = {"kernel_class": kernel_class, "copy_bytes": copy_mib * 2 ** 20,
            "source_sha256": source_hash(kernel_class)}
     for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"),
                                ("write", write_csv, "WRITE_SIZE")):
-        vals = _per_dispatch(path, counter)
-        copy = [v for n, vs in vals.items() if COPY_KERNEL in n for v in vs]
+        disp = [e for e in _dispatches(path) if counter in e["counters"]]
+        copy = [e["counters"][counter] for e in disp if COPY_KERNEL in e["name"]]
         if not copy:
             raise SystemExit(f"no {COPY_KERNEL} dispatch in {path}")
         copy_kib = max(copy)  # the calibration copy is the largest copy dispatch
         scale = (copy_mib * 1024.0) / copy_kib
-        ks = [v for n, vs in vals.items() if pred(n) for v in vs]
+        ks = [e["counters"][counter] for e in disp if e["cls"] == kernel_class]
         if not ks:
             raise SystemExit(f"no {kernel_class} dispatch in {path}")
         res[f"{key}_kib_per_dispatch_raw"] = statistics.fmean(ks)
@@ -123,20 +159,14 @@ def load_traffic(kernel_class: str, workload: str) -> Optional[float]:
 
 def mfma_busy(csv_path: str) -> Dict[str, Dict[str, float]]:
     per: Dict[str, Dict[str, float]] = {}
-    rows = list(csv.DictReader(open(csv_path)))
-    by_dispatch: Dict[Tuple[str, str], Dict[str, float]] = {}
-    for r in rows:
-        key = (r.get("Dispatch_Id", r.get("Correlation_Id", "")), r["Kernel_Name"])
-        by_dispatch.setdefault(key, {})[r["Counter_Name"]] = float(r["Counter_Value"])
-    for (_, name), c in by_dispatch.items():
-        if "SQ_VALU_MFMA_BUSY_CYCLES" not in c or "SQ_BUSY_CU_CYCLES" not in c:
+    for e in _dispatches(csv_path):
+        c = e["counters"]
+        if e["cls"] is None or "SQ_VALU_MFMA_BUSY_CYCLES" not in c or "SQ_BUSY_CU_CYCLES" not in c:
             continue
-        for cls, (_, pred) in KERNEL_CLASSES.items():
-            if pred(name):
-                e = per.setdefault(cls, {"mfma": 0.0, "busy": 0.0, "dispatches": 0})
-                e["mfma"] += c["SQ_VALU_MFMA_BUSY_CYCLES"]
-                e["busy"] += c["SQ_BUSY_CU_CYCLES"]
-                e["dispatches"] += 1
+        v = per.setdefault(e["cls"], {"mfma": 0.0, "busy": 0.0, "dispatches": 0})
+        v["mfma"] += c["SQ_VALU_MFMA_BUSY_CYCLES"]
+        v["busy"] += c["SQ_BUSY_CU_CYCLES"]
+        v["dispatches"] += 1
     return {k: {"mfma_busy_pct": 100.0 * v["mfma"] / (4.0 * v["busy"]) if v["busy"] else 0.0,
                 "dispatches": v["dispatches"]} for k, v in per.items()}
 
@@ -148,16 +178,13 @@ def clock(csv_path: str, nominal_ghz: float = 2.4, peak_tflops: float = 2516.6
     is GRBM_GUI_ACTIVE / 8 / duration.  Also the bf16 MFMA peak at that
     clock (the nominal peak scaled by clock / 2.4 GHz)."""
     per: Dict[str, Dict[str, float]] = {}
-    for r in csv.DictReader(open(csv_path)):
-        if r["Counter_Name"] != "GRBM_GUI_ACTIVE":
+    for e in _dispatches(csv_path):
+        if e["cls"] is None or "GRBM_GUI_ACTIVE" not in e["counters"] or e["ns"] <= 0:
             continue
-        dur = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
-        for cls, (_, pred) in KERNEL_CLASSES.items():
-            if pred(r["Kernel_Name"]) and dur > 0:
-                e = per.setdefault(cls, {"cycles": 0.0, "ns": 0.0, "dispatches": 0})
-                e["cycles"] += float(r["Counter_Value"]) / 8.0
-                e["ns"] += dur
-                e["dispatches"] += 1
+        v = per.setdefault(e["cls"], {"cycles": 0.0, "ns": 0.0, "dispatches": 0})
+        v["cycles"] += e["counters"]["GRBM_GUI_ACTIVE"] / 8.0
+        v["ns"] += e["ns"]
+        v["dispatches"] += 1
     out = {}
     for k, v in per.items():
         ghz = v["cycles"] / v["ns"]
@@ -166,8 +193,43 @@ def clock(csv_path: str, nominal_ghz: float = 2.4, peak_tflops: float = 2516.6
     return out
 
 
+READ_SIZES = {"TCC_EA0_RDREQ_128B_sum": 128.0, "TCC_EA0_RDREQ_64B_sum": 64.0,
+              "TCC_EA0_RDREQ_32B_sum": 32.0}
+
+
+def fabric_reads(csv_path: str) -> Dict[str, Dict[str, float]]:
+    """L2-to-fabric read bytes per launch of each kernel class from a `--pmc
+    TCC_EA0_RDREQ_128B_sum TCC_EA0_RDREQ_64B_sum TCC_EA0_RDREQ_32B_sum
+    TCC_EA0_RDREQ_sum` run: every request counted at its own size, so no
+    calibration copy is needed (FETCH_SIZE's expression takes 128-byte
+    requests from TCC_BUBBLE, which reads 0 on gfx950, and counts them as
+    64 bytes).  `accounted` is the share of all read requests that the three
+    size classes cover."""
+    per: Dict[str, Dict[str, float]] = {}
+    for e in _dispatches(csv_path):
+        c = e["counters"]
+        if e["cls"] is None or not all(k in c for k in READ_SIZES):
+            continue
+        v = per.setdefault(e["cls"], {"bytes": 0.0, "sized": 0.0, "all": 0.0, "dispatches": 0})
+        v["bytes"] += sum(c[k] * b for k, b in READ_SIZES.items())
+        v["sized"] += sum(c[k] for k in READ_SIZES)
+        v["all"] += c.get("TCC_EA0_RDREQ_sum", 0.0)
+        v["dispatches"] += 1
+    return {k: {"dispatches": v["dispatches"], "read_bytes_per_launch": v["bytes"] / v["dispatches"],
+                "accounted": v["sized"] / v["all"] if v["all"] else float("nan")}
+            for k, v in per.items()}
+
+
+def _stored_fetch(kernel_class: str, workload: str) -> Optional[float]:
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel_class}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    return float(json.loads(m.group(1))["fetch_bytes_per_launch"]) if m else None
+
+
 # bench.py kernel names -> traffic class under profiles/
-BENCH_TRAFFIC = {"qkv": "qkv", "ffn1": "ffn1", "oproj": "residual", "ffn2": "residual",
+BENCH_TRAFFIC = {"qkv": "qkv", "ffn1": "ffn1", "oproj": "oproj", "ffn2": "ffn2",
                  "attn": "attn", "ln1": "layernorm", "ln2": "layernorm"}
 MFMA_CLASSES = ("qkv", "oproj", "ffn1", "ffn2")
 
@@ -247,10 +309,14 @@ def main(argv=None):
     k = sub.add_parser("clock")
     k.add_argument("csv")
     k.add_argument("--command", required=True)
+    f = sub.add_parser("fabric")
+    f.add_argument("csv")
+    f.add_argument("--workload", default="bge")
+    f.add_argument("--command", required=True)
     b = sub.add_parser("traffic")
     b.add_argument("fetch_csv")
     b.add_argument("write_csv")
-    b.add_argument("--kernel-class", required=True, choices=sorted(KERNEL_CLASSES))
+    b.add_argument("--kernel-class", required=True, choices=sorted(KERNEL_SOURCES))
     b.add_argument("--copy-mib", type=float, required=True)
     b.add_argument("--command-fetch", required=True)
     b.add_argument("--command-write", required=True)
@@ -267,6 +333,22 @@ def main(argv=None):
                  "| kernel class | dispatches | MFMA busy % |", "|---|---|---|"]
         for k in sorted(res):
             lines.append(f"| {k} | {res[k]['dispatches']} | {res[k]['mfma_busy_pct']:.1f} |")
+        sys.stdout.write("\n".join(lines) + "\n")
+    elif args.cmd == "fabric":
+        res = fabric_reads(args.csv)
+        lines = [f"Command: `{args.command}`", "",
+                 "L2-to-fabric read bytes per launch = 128 x TCC_EA0_RDREQ_128B + 64 x "
+                 "TCC_EA0_RDREQ_64B + 32 x TCC_EA0_RDREQ_32B (summed over the L2 channels and "
+                 "XCDs), averaged over the dispatches of each kernel class; beside it the "
+                 "copy-calibrated FETCH_SIZE figure of the `traffic_*` summaries.", "",
+                 "| kernel class | dispatches | read bytes/launch (request sizes) | "
+                 "FETCH_SIZE x calibration | requests covered by the size classes |",
+                 "|---|---|---|---|---|"]
+        for k in sorted(res):
+            r = res[k]
+            fs = _stored_fetch(k, args.workload)
+            lines.append(f"| {k} | {r['dispatches']} | {r['read_bytes_per_launch']:.4g} | "
+                         f"{'%.4g' % fs if fs else '—'} | {100 * r['accounted']:.2f} % |")
         sys.stdout.write("\n".join(lines) + "\n")
     elif args.cmd == "clock":
         res = clock(args.csv)

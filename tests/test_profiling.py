@@ -16,21 +16,30 @@ ATTN = "void surge::(anonymous namespace)::attention_varlen_kernel<64>(x)"
 COPY = "__amd_rocclr_copyBuffer"
 
 
-def _classes(name):
-    return [c for c, (_, pred) in P.KERNEL_CLASSES.items() if pred(name)]
-
-
 def test_kernel_classification():
     assert P._epi(LIN.format(epi=4, order=1)) == 4
     assert P._epi(ATTN) == -1
-    assert _classes(LIN.format(epi=0, order=0)) == ["qkv"]
-    assert _classes(LIN.format(epi=3, order=0)) == ["qkv"]
-    assert _classes(LIN.format(epi=4, order=1)) == ["ffn1"]
+    assert P.name_class(LIN.format(epi=0, order=0)) == "qkv"
+    assert P.name_class(LIN.format(epi=3, order=0)) == "qkv"
+    assert P.name_class(LIN.format(epi=4, order=1)) == "ffn1"
     for epi in (2, 5, 6):
-        assert _classes(LIN.format(epi=epi, order=0)) == ["residual"]
-    assert _classes(ATTN) == ["attn"]
-    assert _classes("void surge::(anonymous namespace)::ln_rows_kernel<16>(x)") == ["layernorm"]
-    assert _classes(COPY) == []
+        assert P.name_class(LIN.format(epi=epi, order=0)) == "residual"
+    assert P.name_class(ATTN) == "attn"
+    assert P.name_class("void surge::(anonymous namespace)::ln_rows_kernel<16>(x)") == "layernorm"
+    assert P.name_class(COPY) is None
+
+
+def test_residual_gemms_told_apart_by_dispatch_order():
+    """The O-projection and FFN2 share one kernel instance: the one after
+    FFN1 is FFN2, the one after QKV and attention is the O-projection."""
+    qkv0, qkv = LIN.format(epi=0, order=0), LIN.format(epi=3, order=0)
+    o0, res = LIN.format(epi=5, order=0), LIN.format(epi=6, order=0)
+    ffn1 = LIN.format(epi=4, order=1)
+    names = [COPY, "embed_ln_kernel", qkv0, ATTN, o0, ffn1, res,
+             qkv, ATTN, res, ffn1, res, "pool_l2_kernel"]
+    assert P.dispatch_classes(names) == [
+        None, None, "qkv", "attn", "oproj", "ffn1", "ffn2",
+        "qkv", "attn", "oproj", "ffn1", "ffn2", None]
 
 
 def _counter_csv(path, counter, rows):
@@ -155,3 +164,39 @@ def test_roofline_bound_follows_arithmetic_intensity(tmp_path, monkeypatch):
     ffn2 = [l for l in md.splitlines() if l.startswith("| ffn2 ")][0].split("|")
     assert oproj[7].strip() == "hbm" and oproj[9].strip() == f"{100 * 4000 / 8000:.1f}"
     assert ffn2[7].strip() == "mfma" and ffn2[9].strip() == f"{100 * 1000 / 2516.6:.1f}"
+
+
+def test_traffic_of_the_two_residual_gemms(tmp_path):
+    """Counters of O-projection and FFN2 dispatches (one kernel instance)
+    land in their own classes."""
+    fetch = tmp_path / "fetch.csv"
+    write = tmp_path / "write.csv"
+    qkv, res, ffn1 = (LIN.format(epi=3, order=0), LIN.format(epi=6, order=0),
+                      LIN.format(epi=4, order=1))
+    seq = [(COPY, 1024.0), (qkv, 1.0), (ATTN, 1.0), (res, 100.0), (ffn1, 1.0), (res, 300.0),
+           (qkv, 1.0), (ATTN, 1.0), (res, 120.0), (ffn1, 1.0), (res, 340.0)]
+    _counter_csv(fetch, "FETCH_SIZE", seq)
+    _counter_csv(write, "WRITE_SIZE", seq)
+    o = P.traffic(str(fetch), str(write), "oproj", 1.0)
+    f = P.traffic(str(fetch), str(write), "ffn2", 1.0)
+    assert o["fetch_dispatches"] == f["fetch_dispatches"] == 2
+    assert o["fetch_kib_per_dispatch_raw"] == pytest.approx(110.0)
+    assert f["fetch_kib_per_dispatch_raw"] == pytest.approx(320.0)
+    assert o["source_sha256"] == f["source_sha256"] == P.source_hash("ffn1")
+
+
+def test_fabric_reads_count_each_request_at_its_size(tmp_path):
+    path = tmp_path / "fabric.csv"
+    ffn1 = LIN.format(epi=4, order=1)
+    with open(path, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        for d, n128 in enumerate([1000.0, 3000.0]):
+            w.writerow([d, ffn1, "TCC_EA0_RDREQ_128B_sum", n128])
+            w.writerow([d, ffn1, "TCC_EA0_RDREQ_64B_sum", 10.0])
+            w.writerow([d, ffn1, "TCC_EA0_RDREQ_32B_sum", 2.0])
+            w.writerow([d, ffn1, "TCC_EA0_RDREQ_sum", n128 + 12.0])
+    res = P.fabric_reads(str(path))
+    assert res["ffn1"]["dispatches"] == 2
+    assert res["ffn1"]["read_bytes_per_launch"] == pytest.approx(2000.0 * 128 + 640 + 64)
+    assert res["ffn1"]["accounted"] == pytest.approx(1.0)
