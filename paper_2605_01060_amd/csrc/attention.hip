@@ -8,7 +8,7 @@
 // Work decomposition.  A work item is (text, 32-query block); the host
 // lists the items of a chunk longest text first, so the long texts start
 // early and the short ones fill in behind them.  A unit is one item for one
-// head; a wave (a workgroup of its own) handles UNITS_PER_WAVE units,
+// head (or head pair, below); a wave (a workgroup of its own) handles UNITS_PER_WAVE units,
 // grid-strided, walking each unit's keys in 32-key blocks with an online
 // softmax.
 //
@@ -38,6 +38,15 @@
 // is read from the row-major V block with the gfx950 transposing LDS read
 // (ds_read_b64_tr_b16), which hands each lane one feature of 4 consecutive
 // keys.
+//
+// Head pairs.  With 32-dimensional heads a head's slice of a row is only
+// 64 bytes, half a cache line, and a block step has half the MFMA work of a
+// 64-dimensional head for the same softmax work.  So a unit then takes two
+// adjacent heads: its rows are the pair's 128 contiguous bytes, laid out and
+// copied exactly like one 64-dimensional head, while scores, softmax
+// statistics and outputs stay separate per head (each head's arithmetic is
+// the one-head arithmetic, in the same order), and the wave has two
+// independent softmax chains to interleave.
 #include <math.h>
 
 #include "device_common.h"
@@ -51,15 +60,20 @@ namespace {
 // uneven unit costs across CUs (measured best at 4 on the bge workload).
 constexpr int UNITS_PER_WAVE = 4;
 
-template <int DH>
+// DH: bytes / 2 of a unit's row slice (64: one 64-dimensional head or, with
+// PAIR, two adjacent 32-dimensional heads); n_heads counts such slices.
+template <int DH, bool PAIR>
 __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __restrict__ qkv,
                                                               uint16_t* __restrict__ out,
                                                               const int32_t* __restrict__ cu,
                                                               const uint32_t* __restrict__ items,
                                                               int n_heads, float scale_log2,
                                                               int n_units) {
-  constexpr int KSTEPS = DH / 16;  // MFMA steps over the head dimension for S
+  constexpr int KSTEPS = DH / 16;  // MFMA steps over the row slice
   constexpr int DT = DH / 32;      // 32-row tiles of O^T
+  constexpr int NH = PAIR ? 2 : 1; // heads per unit
+  constexpr int KS = KSTEPS / NH;  // MFMA steps over one head for S
+  static_assert(!PAIR || DT == NH, "a head pair owns one O^T tile per head");
   constexpr int CPR = DH / 8;      // 16-byte chunks per row
   constexpr int RPC = 64 / CPR;    // rows one wave copy fills
   constexpr int NCP = 32 / RPC;    // copies per 32-row block
@@ -82,9 +96,9 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
   const uint32_t lv = lds_address(sV[0]);
   constexpr uint32_t BUF = BLK * 16;
 
-  // A unit is (work item, head): item = (text << 7 | 32-query block).
+  // A unit is (work item, row slice h): item = (text << 7 | 32-query block).
   struct Unit {
-    const uint16_t* base;  // Q row of the text's first token, head h
+    const uint16_t* base;  // Q row of the text's first token, slice h
     int q0, L, beg, h;
   };
   auto unit_at = [&](int u) {
@@ -139,9 +153,14 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
 
     bf16x8 qf[KSTEPS];
     u32x4 pv[NCP];
-    float m_run = -INFINITY;  // running max, log2 units (raw score x scale_log2)
-    float l_run = 0.0f;
-    f32x16 o[DT];
+    float m_run[NH];  // running max per head, log2 units (raw score x scale_log2)
+    float l_run[NH];
+#pragma unroll
+    for (int p = 0; p < NH; ++p) {
+      m_run[p] = -INFINITY;
+      l_run[p] = 0.0f;
+    }
+    f32x16 o[DT];  // tile dt belongs to head dt (PAIR) or to the one head
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -186,54 +205,68 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
       const u32x4* kbuf = sK[b];
       const u32x4* vbuf = sV[b];
 
-      // S^T block: rows = keys k0..k0+31 (A operand = K), cols = queries.
-      f32x16 s;
+      // S^T block of each head: rows = keys k0..k0+31 (A operand = K),
+      // cols = queries; head p is steps p*KS .. p*KS+KS-1 of the row slice.
+      f32x16 s[NH];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+      for (int p = 0; p < NH; ++p) {
 #pragma unroll
-      for (int kk = 0; kk < KSTEPS; ++kk)
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8, kbuf[swz<CPR>(col, kk * 2 + half)]), qf[kk], s, 0, 0, 0);
+        for (int r = 0; r < 16; ++r) s[p][r] = 0.0f;
+#pragma unroll
+        for (int kk = p * KS; kk < (p + 1) * KS; ++kk)
+          s[p] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, kbuf[swz<CPR>(col, kk * 2 + half)]), qf[kk], s[p], 0, 0, 0);
+      }
 
       // Register r holds the score of key k0 + 8*(r/4) + 4*half + r%4; only
       // the text's last block has keys past its end (uniform branch).
       if (k0 + 32 > cur.L) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (k0 + 8 * (r >> 2) + 4 * half + (r & 3) >= cur.L) s[r] = -INFINITY;
-      }
-      float mloc = s[0];
+        for (int p = 0; p < NH; ++p)
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[r]);
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run, mloc * scale_log2);
-      float psum = 0.0f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -m_new));
-        psum += s[r];
+          for (int r = 0; r < 16; ++r)
+            if (k0 + 8 * (r >> 2) + 4 * half + (r & 3) >= cur.L) s[p][r] = -INFINITY;
       }
-      psum += __shfl_xor(psum, 32, 64);
-      if (kb == 0) {
-        l_run = psum;  // o is still zero: nothing to rescale
-      } else {
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run = fmaf(l_run, alpha, psum);
+      float alpha[NH];
+#pragma unroll
+      for (int p = 0; p < NH; ++p) {
+        float mloc = s[p][0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) mloc = fmaxf(mloc, s[p][r]);
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        const float m_new = fmaxf(m_run[p], mloc * scale_log2);
+        float psum = 0.0f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[p][r] = __builtin_amdgcn_exp2f(fmaf(s[p][r], scale_log2, -m_new));
+          psum += s[p][r];
+        }
+        psum += __shfl_xor(psum, 32, 64);
+        if (kb == 0) {
+          l_run[p] = psum;  // o is still zero: nothing to rescale
+        } else {
+          alpha[p] = __builtin_amdgcn_exp2f(m_run[p] - m_new);
+          l_run[p] = fmaf(l_run[p], alpha[p], psum);
+        }
+        m_run[p] = m_new;
+      }
+      if (kb > 0) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha[PAIR ? dt : 0];
       }
-      m_run = m_new;
 
       // O^T += V^T P^T over two 16-key halves c: slot j of this lane is key
       // 16c + 8*(j/4) + 4*half + j%4, the same key for the P (B) and V (A)
       // operands.
-      bf16x8 pb[2];
+      bf16x8 pb[NH][2];
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+      for (int p = 0; p < NH; ++p)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) pb[c][j] = (__bf16)s[8 * c + j];
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) pb[p][c][j] = (__bf16)s[p][8 * c + j];
       const char* vbytes = reinterpret_cast<const char*>(vbuf);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
@@ -249,7 +282,7 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
                                                    (__attribute__((address_space(3))) i16x4*)pa));
           }
           const bf16x8 va = __builtin_shufflevector(v2[0], v2[1], 0, 1, 2, 3, 4, 5, 6, 7);
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[c], o[dt], 0, 0, 0);
+          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[PAIR ? dt : 0][c], o[dt], 0, 0, 0);
         }
       }
       b ^= 1;
@@ -258,15 +291,18 @@ __global__ __launch_bounds__(64) void attention_varlen_kernel(const uint16_t* __
     // O^T register r of tile dt: head feature dt*32 + 8*(r/4) + 4*half + r%4
     // of query q0 + col.  Stage the normalised bf16 block in the K buffer of
     // the unit's last key block (row = query; its K reads went into MFMAs).
-    const float inv = 1.0f / l_run;
+    float inv[NH];
+#pragma unroll
+    for (int p = 0; p < NH; ++p) inv[p] = 1.0f / l_run[p];
     char* obytes = reinterpret_cast<char*>(sK[b ^ 1]);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const float inv_h = inv[PAIR ? dt : 0];
         uint2 w;
-        w.x = pack_bf16x2(o[dt][4 * g + 0] * inv, o[dt][4 * g + 1] * inv);
-        w.y = pack_bf16x2(o[dt][4 * g + 2] * inv, o[dt][4 * g + 3] * inv);
+        w.x = pack_bf16x2(o[dt][4 * g + 0] * inv_h, o[dt][4 * g + 1] * inv_h);
+        w.y = pack_bf16x2(o[dt][4 * g + 2] * inv_h, o[dt][4 * g + 3] * inv_h);
         *reinterpret_cast<uint2*>(obytes + swz<CPR>(col, dt * 4 + g) * 16 + half * 8) = w;
       }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -297,15 +333,18 @@ hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* c
                             const uint32_t* items, int n_items, int n_heads, int d_head,
                             hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
+  if (d_head != 64 && (d_head != 32 || n_heads % 2)) return hipErrorInvalidValue;
   const float scale_log2 = 1.4426950408889634f / sqrtf((float)d_head);
-  const int n_units = n_items * n_heads;
+  // 32-dimensional heads go in adjacent pairs: one 64-wide row slice each.
+  const int slices = d_head == 64 ? n_heads : n_heads / 2;
+  const int n_units = n_items * slices;
   const dim3 grid((unsigned)((n_units + UNITS_PER_WAVE - 1) / UNITS_PER_WAVE));
   if (d_head == 64)
-    hipLaunchKernelGGL(attention_varlen_kernel<64>, grid, dim3(64), 0, stream, qkv, out, cu, items,
-                       n_heads, scale_log2, n_units);
+    hipLaunchKernelGGL((attention_varlen_kernel<64, false>), grid, dim3(64), 0, stream, qkv, out, cu,
+                       items, slices, scale_log2, n_units);
   else
-    hipLaunchKernelGGL(attention_varlen_kernel<32>, grid, dim3(64), 0, stream, qkv, out, cu, items,
-                       n_heads, scale_log2, n_units);
+    hipLaunchKernelGGL((attention_varlen_kernel<64, true>), grid, dim3(64), 0, stream, qkv, out, cu,
+                       items, slices, scale_log2, n_units);
   return hipGetLastError();
 }
 

@@ -223,7 +223,7 @@ def test_linear_fused_full_chunk_sampled_rows(epi, N, K):
 ATTN_LENGTHS = [1, 2, 3, 4, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 255, 256, 511, 512]
 
 
-@pytest.mark.parametrize("n_heads,d_head", [(2, 64), (12, 32), (12, 64), (16, 64)])
+@pytest.mark.parametrize("n_heads,d_head", [(2, 64), (4, 32), (12, 32), (12, 64), (16, 64)])
 def test_attention_packed_mixed_lengths(n_heads, d_head):
     torch = torch_cuda()
     rng = np.random.default_rng(n_heads * 100 + d_head)
@@ -247,12 +247,14 @@ def test_attention_packed_mixed_lengths(n_heads, d_head):
     print(f"[attention {n_heads}x{d_head}] max err {worst:.3e}")
 
 
-def test_attention_no_cross_text_leak():
-    """Two texts whose values differ by a large constant: any attention to
-    the other text would pull outputs away from the text's own value range."""
+@pytest.mark.parametrize("n_heads,d_head", [(12, 64), (12, 32), (4, 32)])
+def test_attention_no_cross_text_leak(n_heads, d_head):
+    """Texts whose values differ by a large constant: any attention to
+    another text would pull outputs away from the text's own value range
+    (32-dimensional heads run in adjacent pairs, so this also covers the
+    pair path)."""
     torch = torch_cuda()
     rng = np.random.default_rng(5)
-    n_heads, d_head = 12, 64
     d = n_heads * d_head
     lengths = [40, 70, 33]
     cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
