@@ -20,8 +20,9 @@
 // has arrived, so every wait is for "everything issued so far" and no wait
 // depends on how many stores were issued.
 //
-// Memory path.  A head's slice of a token row is DH contiguous bf16 (128 B
-// for DH = 64).  Q, K and V blocks move from global memory to LDS with
+// Memory path.  A unit's slice of a token row is 64 contiguous bf16, 128
+// bytes (one 64-dimensional head, or a pair of 32-dimensional heads as
+// below).  Q, K and V blocks move from global memory to LDS with
 // direct copies that read whole rows (8 lanes per 128-byte row), stored in
 // the conflict-free chunk swizzle; the next K/V block is copied into the
 // second LDS buffer while the current one is on the MFMA units.  The output
