@@ -26,8 +26,8 @@ extern "C" {
  * every text): out[t] = LN(word[id_t] + pos[t - cu_i]).
  * d_tokens int32 [cu[n]]; d_word bf16 [vocab, d]; d_pos bf16 [max_pos, d];
  * gamma/beta fp32 [d]; d_out bf16 [cu[n], d].  d % 128 == 0, d <= 1024,
- * every text length <= max_pos.  Out-of-vocabulary IDs are read as ID 0 and
- * reported with SURGE_ERR_INVALID_ARGUMENT after the stage ran.
+ * every text length <= min(max_pos, 4096).  Out-of-vocabulary IDs are read
+ * as ID 0 and reported with SURGE_ERR_INVALID_ARGUMENT after the stage ran.
  */
 surge_status surge_op_embed_ln(int64_t n_texts, const int64_t* h_cu_seqlens, const int32_t* d_tokens,
                                const uint16_t* d_word, int32_t vocab, const uint16_t* d_pos,

@@ -349,7 +349,7 @@ hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* c
   return hipGetLastError();
 }
 
-int attention_items(const int64_t* cu, int64_t n_texts, uint32_t* items) {
+int row_block_items(const int64_t* cu, int64_t n_texts, uint32_t* items) {
   // (text, query block) pairs, longest text first; ties keep text order.
   int64_t n = 0;
   int64_t maxL = 0;

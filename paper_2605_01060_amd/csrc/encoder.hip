@@ -191,7 +191,7 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
     memcpy(hdst, e->h_dst.data() + t0, (size_t)S * 8);
     e->h_lcu.resize((size_t)S + 1);
     for (int64_t i = 0; i <= S; ++i) e->h_lcu[(size_t)i] = cu[t0 + i] - cu[t0];
-    const int n_items = attention_items(e->h_lcu.data(), S, hitems);
+    const int n_items = row_block_items(e->h_lcu.data(), S, hitems);
     const size_t cu_bytes = align_up((size_t)(S + 1) * 4, 16);
     HIP_TRY(hipMemcpyAsync(e->d_cu, hcu, cu_bytes, hipMemcpyHostToDevice, stream));
     HIP_TRY(hipMemcpyAsync(e->d_dst, hdst, (size_t)S * 8, hipMemcpyHostToDevice, stream));
@@ -209,8 +209,8 @@ surge_status encode_chunks(surge_encoder* e, int64_t n_texts, const int32_t* d_t
     const int Si = (int)S;
 
     LAUNCH(SURGE_KERNEL_EMBED, 0.0, Td * (4.0 + 6.0 * d),
-           launch_embed_ln(toks, e->d_cu, Si, e->word, e->pos, e->lneg, e->lneb, D.ln_eps,
-                           D.vocab_size, d, e->X, e->d_err, stream));
+           launch_embed_ln(toks, e->d_cu, e->d_items, n_items, e->word, e->pos, e->lneg,
+                           e->lneb, D.ln_eps, D.vocab_size, d, e->X, e->d_err, stream));
     // Post-LN with the LayerNorms folded into their neighbours: X and Y
     // hold raw (pre-LN) residual rows, SX and SY their statistics partials
     // (written by the residual GEMMs), RX and RY the per-row factors.

@@ -8,13 +8,14 @@
 
 namespace surge {
 
-// x_t = LN(word[id_t] + pos[t - cu_i]) for every token of n_texts texts.
-// tokens [cu[n_texts]], cu int32 [n_texts+1] (device), out bf16 [T, d].
-// Out-of-vocabulary IDs are gathered as ID 0 and set *err = 1.
-hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts,
-                           const uint16_t* word, const uint16_t* pos, const float* gamma,
-                           const float* beta, float eps, int vocab, int d, uint16_t* out, int* err,
-                           hipStream_t stream);
+// x_t = LN(word[id_t] + pos[t - cu_i]) for every token.  tokens [T],
+// cu int32 [n_texts+1] and the row_block_items work items (device), one
+// workgroup per item; out bf16 [T, d].  Out-of-vocabulary IDs are gathered
+// as ID 0 and set *err = 1.
+hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, const uint32_t* items,
+                           int n_items, const uint16_t* word, const uint16_t* pos,
+                           const float* gamma, const float* beta, float eps, int vocab, int d,
+                           uint16_t* out, int* err, hipStream_t stream);
 
 // Y[M, N] = epi(X[M, K] W^T + b), W stored [N, K] (out, in), bf16 in/out.
 // Requires N % 128 == 0, K % 64 == 0, M >= 1.
@@ -65,14 +66,16 @@ int linear_stats_width(int64_t M, int N);
 // Packed varlen multi-head self-attention.  qkv bf16 [T, 3 H dh] (Q | K | V
 // column blocks, head h at columns h*dh of each), out bf16 [T, H dh].
 // Attention runs within each text only.  dh is 32 or 64.  items lists the
-// (text << 7 | 32-query block) work items built by attention_items.
+// (text << 7 | 32-row block) work items built by row_block_items.
 hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* cu,
                             const uint32_t* items, int n_items, int n_heads, int d_head,
                             hipStream_t stream);
 
-// Work items of a chunk (at most cu[n_texts] of them, every text length in
-// [1, 4096]), longest text first.  Returns the item count.
-int attention_items(const int64_t* cu, int64_t n_texts, uint32_t* items);
+// Work items of a chunk: (text << 7 | block) for every block of 32
+// consecutive rows of a text (the attention's query blocks, the
+// embedding's row blocks); at most cu[n_texts] of them, every text length
+// in [1, 4096]; longest text first.  Returns the item count.
+int row_block_items(const int64_t* cu, int64_t n_texts, uint32_t* items);
 
 // Per-row LayerNorm factors rows[m] = (rstd, -mean * rstd) from `parts`
 // equal-width statistics partials stats[p * M + m] = (mean, variance).

@@ -1,6 +1,7 @@
 // Stage-level entry points: one kernel of the encode path on caller buffers.
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <vector>
 
@@ -98,16 +99,21 @@ surge_status surge_op_embed_ln(int64_t n_texts, const int64_t* cu, const int32_t
     return fail(SURGE_ERR_INVALID_ARGUMENT, "device buffers must be 16-byte aligned");
   DeviceCu dcu;
   int64_t T = 0;
-  surge_status st = upload_cu(n_texts, cu, max_pos, &dcu, &T);
+  surge_status st = upload_cu(n_texts, cu, std::min(max_pos, 4096), &dcu, &T);
   if (st != SURGE_OK) return st;
+  std::vector<uint32_t> items((size_t)T);
+  const int n_items = row_block_items(cu, n_texts, items.data());
+  DeviceCu ditems;
+  HIP_TRY(hipMalloc(&ditems.ptr, (size_t)n_items * 4));
+  HIP_TRY(hipMemcpy(ditems.ptr, items.data(), (size_t)n_items * 4, hipMemcpyHostToDevice));
   int* derr = nullptr;
   HIP_TRY(hipMalloc(&derr, sizeof(int)));
   DeviceCu guard;  // frees derr through the same path
   guard.ptr = (int32_t*)derr;
   HIP_TRY(hipMemset(derr, 0, sizeof(int)));
   hipStream_t s = (hipStream_t)hip_stream;
-  HIP_TRY(launch_embed_ln(d_tokens, dcu.ptr, (int)n_texts, d_word, d_pos, d_gamma, d_beta, eps,
-                          vocab, d, d_out, derr, s));
+  HIP_TRY(launch_embed_ln(d_tokens, dcu.ptr, (const uint32_t*)ditems.ptr, n_items, d_word, d_pos,
+                          d_gamma, d_beta, eps, vocab, d, d_out, derr, s));
   HIP_TRY(hipStreamSynchronize(s));
   int flag = 0;
   HIP_TRY(hipMemcpy(&flag, derr, sizeof(int), hipMemcpyDeviceToHost));
@@ -258,7 +264,7 @@ surge_status surge_op_attention(int64_t n_texts, const int64_t* cu, int32_t n_he
   surge_status st = upload_cu(n_texts, cu, 4096, &dcu, &T);
   if (st != SURGE_OK) return st;
   std::vector<uint32_t> items((size_t)T);
-  const int n_items = attention_items(cu, n_texts, items.data());
+  const int n_items = row_block_items(cu, n_texts, items.data());
   DeviceCu ditems;
   HIP_TRY(hipMalloc(&ditems.ptr, (size_t)n_items * 4));
   HIP_TRY(hipMemcpy(ditems.ptr, items.data(), (size_t)n_items * 4, hipMemcpyHostToDevice));

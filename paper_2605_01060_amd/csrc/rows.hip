@@ -59,20 +59,25 @@ __device__ __forceinline__ void ln_row(float (&v)[MAXC][8], int nch, int lane, i
   }
 }
 
-// One block per text; its four waves take the text's tokens in turn.  A
-// wave fetches its next row's token ID and table chunks before it
+// One block per work item (text t, rows 32b .. 32b+31 of it), so a long
+// text is spread over several blocks instead of keeping one block busy to
+// the end of the launch; the block's four waves take the item's rows in
+// turn.  A wave fetches its next row's token ID and table chunks before it
 // normalises the current row, so one row's gather latency hides behind the
 // previous row's work.
 __global__ __launch_bounds__(256) void embed_ln_kernel(
     const int32_t* __restrict__ tokens, const int32_t* __restrict__ cu,
-    const uint16_t* __restrict__ word, const uint16_t* __restrict__ pos,
-    const float* __restrict__ gamma, const float* __restrict__ beta, float eps, int vocab, int d,
-    uint16_t* __restrict__ out, int* __restrict__ err) {
-  const int t = blockIdx.x;
+    const uint32_t* __restrict__ items, const uint16_t* __restrict__ word,
+    const uint16_t* __restrict__ pos, const float* __restrict__ gamma,
+    const float* __restrict__ beta, float eps, int vocab, int d, uint16_t* __restrict__ out,
+    int* __restrict__ err) {
+  const uint32_t item = items[blockIdx.x];
+  const int t = (int)(item >> 7);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int beg = cu[t];
-  const int L = cu[t + 1] - beg;
+  const int r0 = (int)(item & 127u) * 32;           // first row of the item
+  const int r1 = min(r0 + 32, cu[t + 1] - beg);     // one past its last
   const int nch = d >> 3;
   // Table chunks of row p (word row of its checked ID, position row p).
   auto fetch = [&](int p, uint4 (&w)[MAXC], uint4 (&q)[MAXC]) {
@@ -93,8 +98,8 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(
     }
   };
   uint4 wn[MAXC], qn[MAXC];
-  if (wave < L) fetch(wave, wn, qn);
-  for (int p = wave; p < L; p += 4) {
+  if (r0 + wave < r1) fetch(r0 + wave, wn, qn);
+  for (int p = r0 + wave; p < r1; p += 4) {
     float v[MAXC][8];
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
@@ -106,7 +111,7 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(
         for (int e = 0; e < 8; ++e) v[c][e] = a[e] + b[e];
       }
     }
-    if (p + 4 < L) fetch(p + 4, wn, qn);
+    if (p + 4 < r1) fetch(p + 4, wn, qn);
     ln_row(v, nch, lane, d, gamma, beta, eps, out + (size_t)(beg + p) * d);
   }
 }
@@ -252,13 +257,13 @@ __global__ __launch_bounds__(256) void ln_rows_kernel(const float2* __restrict__
 
 }  // namespace
 
-hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, int n_texts,
-                           const uint16_t* word, const uint16_t* pos, const float* gamma,
-                           const float* beta, float eps, int vocab, int d, uint16_t* out, int* err,
-                           hipStream_t stream) {
-  if (n_texts <= 0) return hipSuccess;
-  hipLaunchKernelGGL(embed_ln_kernel, dim3(n_texts), dim3(256), 0, stream, tokens, cu, word, pos,
-                     gamma, beta, eps, vocab, d, out, err);
+hipError_t launch_embed_ln(const int32_t* tokens, const int32_t* cu, const uint32_t* items,
+                           int n_items, const uint16_t* word, const uint16_t* pos,
+                           const float* gamma, const float* beta, float eps, int vocab, int d,
+                           uint16_t* out, int* err, hipStream_t stream) {
+  if (n_items <= 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_ln_kernel, dim3(n_items), dim3(256), 0, stream, tokens, cu, items, word,
+                     pos, gamma, beta, eps, vocab, d, out, err);
   return hipGetLastError();
 }
 
