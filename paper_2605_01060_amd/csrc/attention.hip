@@ -350,7 +350,7 @@ hipError_t launch_attention(const uint16_t* qkv, uint16_t* out, const int32_t* c
 }
 
 int row_block_items(const int64_t* cu, int64_t n_texts, uint32_t* items) {
-  // (text, query block) pairs, longest text first; ties keep text order.
+  // (text, 32-row block) pairs, longest text first; ties keep text order.
   int64_t n = 0;
   int64_t maxL = 0;
   for (int64_t i = 0; i < n_texts; ++i) maxL = cu[i + 1] - cu[i] > maxL ? cu[i + 1] - cu[i] : maxL;
