@@ -311,6 +311,43 @@ def test_embed_ln(d):
         assert np.all(err <= BF16_REL * np.abs(ref) + 1e-4), (i, float(err.max()))
 
 
+def test_rows_at_the_4096_token_limit():
+    """A 4096-token text is 128 blocks of 32 rows, the most a work item's
+    7-bit block index holds: embedding and attention (32- and
+    64-dimensional heads) must cover every row of it."""
+    torch = torch_cuda()
+    rng = np.random.default_rng(4096)
+    d, vocab, max_pos = 128, 500, 4096
+    lengths = [4096, 3, 40]
+    cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    T = int(cu[-1])
+    word, w64 = _bf16(torch, rng.standard_normal((vocab, d)) * 0.02)
+    pos, p64 = _bf16(torch, rng.standard_normal((max_pos, d)) * 0.02)
+    g64 = (1.0 + 0.02 * rng.standard_normal(d)).astype(np.float32).astype(np.float64)
+    b64 = (0.02 * rng.standard_normal(d)).astype(np.float32).astype(np.float64)
+    ids = rng.integers(0, vocab, size=T).astype(np.int32)
+    out = torch.full((T, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    S.surge_op_embed_ln(cu, torch.from_numpy(ids).cuda(), word, vocab, pos, max_pos,
+                        _f32(torch, g64), _f32(torch, b64), 1e-12, d, out)
+    got = _to_np(out)
+    wd = {"word_emb": w64, "pos_emb": p64, "ln_e_g": g64, "ln_e_b": b64}
+    for i in range(len(lengths)):
+        a, b_ = int(cu[i]), int(cu[i + 1])
+        ref = E.embed(wd, ids[a:b_].astype(np.int64), 1e-12)
+        assert np.all(np.abs(got[a:b_] - ref) <= BF16_REL * np.abs(ref) + 1e-4), i
+    for n_heads, d_head in ((2, 64), (4, 32)):
+        qkv, q64 = _bf16(torch, rng.standard_normal((T, 3 * d)))
+        att = torch.full((T, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+        S.surge_op_attention(cu, n_heads, d_head, qkv, att)
+        got = _to_np(att)
+        assert not np.isnan(got).any()
+        for i in range(len(lengths)):
+            a, b_ = int(cu[i]), int(cu[i + 1])
+            ref = E.self_attention(q64[a:b_], n_heads)
+            err = np.abs(got[a:b_] - ref)
+            assert np.all(err <= BF16_REL * np.abs(ref) + 1.5e-2), (n_heads, i, float(err.max()))
+
+
 def test_embed_ln_reports_out_of_vocab_ids():
     torch = torch_cuda()
     d, vocab, max_pos = 128, 50, 8
